@@ -1,0 +1,218 @@
+/*
+ * kara.h -- C ABI of libkara, the MI355X (gfx950) implementation of Kara's
+ * sliding-window KV-cache compression step (Kara, Sec. 4 and App. C).
+ *
+ * One compression event, for every triggered sequence, every layer and every
+ * KV head ("unit"), runs:
+ *   1. window scoring, Eq. (4): bidirectional (unmasked) attention of the
+ *      |W| window queries over the |W|-|U| compressible window keys, softmax
+ *      over keys, column sum over queries.  With grouped-query attention the
+ *      G = n_q_heads / n_kv_heads query heads sharing a KV head are all
+ *      queries of that head (G*|W| query rows per unit);
+ *   2. discrete top-k, Eq. (5): budget - alpha positions;
+ *   3. Token2Chunk, Eq. (6)-(8), then the fill rule of App. C.3: exactly
+ *      `budget` kept positions per unit;
+ *   4. the window gather, Eq. (9), done in place in the paged cache (memory
+ *      compaction of Algorithm 1), and the metadata update: trailing pages
+ *      released, block table and sequence length rewritten.
+ *
+ * Conventions
+ *   - Every array pointer is DEVICE memory owned by the caller, except the
+ *     `k_pools` / `v_pools` arrays themselves, which are HOST arrays of
+ *     `n_layers` device pointers.  The library allocates nothing.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Calls only enqueue
+ *     work; none synchronises.
+ *   - Return codes report host-checkable argument errors only; on error
+ *     nothing is enqueued.  Data-dependent problems of a triggered sequence
+ *     (window outside the sequence, page id outside the pool, the sequence
+ *     triggered twice, sequence index out of range) are written to the
+ *     device array `status[t]` (KARA_SEQ_* bits); such a sequence gets zero
+ *     scores and is neither compacted nor committed.
+ *   - kara_token2chunk writes -1 to every kept entry of a unit whose discrete
+ *     row is not strictly ascending inside [0, window - buffer).
+ *   - Ordering: every ranking is by (value descending, index ascending).
+ *
+ * Layouts (row-major, contiguous)
+ *   q            [n_layers][n_trig][window][n_q_heads][head_dim]   bf16|f32
+ *                query head hq = kv_head * G + g belongs to KV head kv_head.
+ *   pools        per layer [num_pages][n_kv_heads][block_size][head_dim]
+ *   block_table  [n_seqs][max_blocks_per_seq] int32, -1 = no page
+ *   seq_lens, win_start  [n_seqs] int32; the window of sequence s covers
+ *                logical positions [win_start[s], win_start[s] + window);
+ *                positions [win_start+window, seq_len) are the tail that
+ *                follows the window.  win_start need not be block aligned.
+ *   trig         [n_trig] int32 sequence indices compressed by this call
+ *   scores       [n_layers][n_trig][n_kv_heads][window - buffer]    f32
+ *   discrete     [n_layers][n_trig][n_kv_heads][budget - chunk_budget] int32,
+ *                ascending window-relative positions
+ *   kept         [n_layers][n_trig][n_kv_heads][budget] int32, ascending
+ *   status       [n_trig] int32
+ *   freed        [n_trig][max_blocks_per_seq] int32 page ids released, in
+ *                ascending logical-block order, -1 after the last one
+ *   n_freed      [n_trig] int32
+ *
+ * Unit u = (layer * n_trig + t) * n_kv_heads + kv_head.
+ */
+#ifndef KARA_H
+#define KARA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KARA_ABI_VERSION 1
+
+/* Largest compressible region |W|-|U| one call supports. */
+#define KARA_MAX_COMPRESSIBLE 4096
+
+typedef enum kara_dtype {
+  KARA_BF16 = 0, /* raw bfloat16, 2 bytes */
+  KARA_F32 = 1   /* IEEE binary32 */
+} kara_dtype_t;
+
+typedef enum kara_status {
+  KARA_OK = 0,
+  KARA_ERR_INVALID_ARG = -1, /* a parameter is out of range or a pointer is NULL */
+  KARA_ERR_UNSUPPORTED = -2, /* valid but not built (e.g. head_dim not 64/128) */
+  KARA_ERR_WORKSPACE = -3,   /* workspace missing or smaller than kara_workspace_size() */
+  KARA_ERR_HIP = -4          /* the HIP runtime rejected a launch */
+} kara_status_t;
+
+/* Per-sequence device status bits. */
+#define KARA_SEQ_OK 0
+#define KARA_SEQ_BAD_WINDOW 1   /* win_start < 0, win_start + window > seq_len, or seq_len > table capacity */
+#define KARA_SEQ_BAD_PAGE 2     /* a page id of the window or tail is outside [0, num_pages) */
+#define KARA_SEQ_DUP_TRIGGER 4  /* the sequence appears more than once in trig */
+#define KARA_SEQ_BAD_INDEX 8    /* trig[t] outside [0, n_seqs) */
+#define KARA_SEQ_BAD_KEPT 16    /* kara_compact_pages: a kept row not ascending or outside [0, window-buffer) */
+
+/*
+ * Window and cache geometry (Kara Sec. 4.1, Eq. (5) and (7); App. C.4).
+ *   window          |W| >= 1
+ *   buffer          |U|, 0 <= U < W; window - buffer <= KARA_MAX_COMPRESSIBLE
+ *   budget          ceil(r (|W|-|U|)): positions kept per unit, 1..W-U
+ *   chunk_budget    alpha, 0 <= alpha < budget
+ *   max_chunk_len   gamma >= 3, chunk length counting both endpoints
+ *   head_dim        d, 64 or 128
+ *   n_q_heads, n_kv_heads   n_q_heads a multiple of n_kv_heads
+ *   block_size      tokens per page, >= 1
+ *   num_pages       pages in each pool
+ *   max_blocks_per_seq, n_seqs   block-table shape
+ *   dtype           KARA_BF16 or KARA_F32 (q and the pools)
+ *   scale           logit scale; <= 0 means 1/sqrt(head_dim) (Eq. (1))
+ */
+typedef struct kara_params {
+  int32_t window;
+  int32_t buffer;
+  int32_t budget;
+  int32_t chunk_budget;
+  int32_t max_chunk_len;
+  int32_t head_dim;
+  int32_t n_q_heads;
+  int32_t n_kv_heads;
+  int32_t block_size;
+  int32_t num_pages;
+  int32_t max_blocks_per_seq;
+  int32_t n_seqs;
+  int32_t dtype;
+  float scale;
+} kara_params_t;
+
+/* Human-readable name of a kara_status_t value.  Never NULL. */
+const char* kara_status_string(int32_t status);
+
+/* KARA_ABI_VERSION of the loaded library. */
+int32_t kara_abi_version(void);
+
+/*
+ * Bytes of device workspace kara_score_window / kara_compress_window need for
+ * this geometry, n_trig triggered sequences and n_layers layers (written to
+ * *bytes, a HOST pointer).  Holds partial column sums of Eq. (4) and, for
+ * outputs the caller does not request, the scores and index sets.
+ */
+kara_status_t kara_workspace_size(const kara_params_t* p, int32_t n_trig, int32_t n_layers,
+                                  size_t* bytes);
+
+/*
+ * Checks every triggered sequence's window against its length and block
+ * table and writes status[t] (KARA_SEQ_* bits).  Reads block_table,
+ * seq_lens, win_start; writes status.
+ */
+kara_status_t kara_validate(const kara_params_t* p, int32_t n_trig, const int32_t* trig,
+                            const int32_t* block_table, const int32_t* seq_lens,
+                            const int32_t* win_start, int32_t* status, void* stream);
+
+/*
+ * Window scoring, Eq. (4), for n_layers layers: writes scores (fp32) and
+ * status.  The key states are read from k_pools through the block table.
+ * Reductions run in a fixed order, so results are bit-reproducible.
+ */
+kara_status_t kara_score_window(const kara_params_t* p, int32_t n_trig, const int32_t* trig,
+                                int32_t n_layers, const void* q, const void* const* k_pools,
+                                const int32_t* block_table, const int32_t* seq_lens,
+                                const int32_t* win_start, float* scores, int32_t* status,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Discrete top-k, Eq. (5): for each of n_units score rows (window - buffer
+ * fp32 values), writes the budget - chunk_budget best positions, ascending.
+ */
+kara_status_t kara_select(const kara_params_t* p, int64_t n_units, const float* scores,
+                          int32_t* discrete, void* stream);
+
+/*
+ * Token2Chunk, Eq. (6)-(8), and the fill rule of App. C.3: from each unit's
+ * scores and ascending discrete set, writes the `budget` kept positions,
+ * ascending.  Chunk scores are formed in fp64 from the fp32 scores.
+ */
+kara_status_t kara_token2chunk(const kara_params_t* p, int64_t n_units, const float* scores,
+                               const int32_t* discrete, int32_t* kept, void* stream);
+
+/*
+ * Window gather, Eq. (9), in place in the paged pools of n_layers layers:
+ * window-relative row j receives row kept[j] for j < budget, then the buffer
+ * rows, then the tail rows (each K and V head independently).  Writes status
+ * (validation runs first).  Does not touch block_table or seq_lens: call
+ * kara_commit_tables once after every layer has been compacted.  Compacting
+ * the same layer twice before committing is a caller error.
+ */
+kara_status_t kara_compact_pages(const kara_params_t* p, int32_t n_trig, const int32_t* trig,
+                                 int32_t n_layers, const int32_t* kept, void* const* k_pools,
+                                 void* const* v_pools, const int32_t* block_table,
+                                 const int32_t* seq_lens, const int32_t* win_start,
+                                 int32_t* status, void* stream);
+
+/*
+ * Metadata update of Algorithm 1: new seq_len = seq_len - (window - buffer -
+ * budget); the logical blocks no longer covered are released (page ids into
+ * freed[t][*] in ascending block order, table entries set to -1).  Writes
+ * status (validation runs first); flagged sequences are left unchanged.
+ */
+kara_status_t kara_commit_tables(const kara_params_t* p, int32_t n_trig, const int32_t* trig,
+                                 int32_t* block_table, int32_t* seq_lens,
+                                 const int32_t* win_start, int32_t* freed, int32_t* n_freed,
+                                 int32_t* status, void* stream);
+
+/*
+ * The whole step (Kara Sec. 4, Algorithm 1) for n_layers layers: validation,
+ * scoring, selection, Token2Chunk + fill, in-place compaction and -- when
+ * `commit` is non-zero -- the metadata update.  scores, discrete and kept are
+ * optional outputs (NULL: kept in the workspace).  freed/n_freed are needed
+ * only when commit is non-zero.
+ */
+kara_status_t kara_compress_window(const kara_params_t* p, int32_t n_trig, const int32_t* trig,
+                                   int32_t n_layers, const void* q, void* const* k_pools,
+                                   void* const* v_pools, int32_t* block_table, int32_t* seq_lens,
+                                   const int32_t* win_start, int32_t commit, float* scores,
+                                   int32_t* discrete, int32_t* kept, int32_t* freed,
+                                   int32_t* n_freed, int32_t* status, void* workspace,
+                                   size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KARA_H */

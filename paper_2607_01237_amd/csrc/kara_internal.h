@@ -1,0 +1,73 @@
+// Internal declarations shared by libkara's host API and its gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kara.h"
+
+namespace kara {
+
+// Most layers one launch addresses (their pool pointers travel as kernel
+// arguments); larger calls are split into several launches.
+constexpr int kMaxLayersPerLaunch = 64;
+
+// Geometry as the kernels see it (derived once on the host).
+struct Geom {
+  int W, U, N;          // window, buffer, compressible length N = W - U
+  int budget, alpha, gamma;
+  int k_disc;           // budget - alpha, Eq. (5)
+  int n_chunks;         // floor(alpha / (gamma - 2)), Eq. (7)
+  int d, Hq, Hkv, G;    // head dim, query heads, KV heads, group size
+  int bs, num_pages, max_blocks, n_seqs;
+  int dtype;            // KARA_BF16 | KARA_F32
+  int esize;            // element bytes
+  float scale;          // logit scale of Eq. (1)
+  int n_trig;
+};
+
+struct PoolPtrs {
+  void* p[kMaxLayersPerLaunch];
+};
+
+// Validation kernel (kara_validate.hip).
+hipError_t launch_validate(const Geom& g, const int32_t* trig, const int32_t* block_table,
+                           const int32_t* seq_lens, const int32_t* win_start, int32_t* status,
+                           hipStream_t stream);
+
+// Scoring (kara_score.hip): partial column sums, one slab per row split.
+struct ScorePlan {
+  int cg, rg, nt;       // column groups, row groups, 16-key tiles per wave
+  int n_rb;             // 16*rg-row blocks per unit
+  int n_splits;         // row splits per unit
+  int n_cols;           // padded column count cg * nt * 16
+};
+ScorePlan plan_score(const Geom& g, int64_t n_units);
+hipError_t launch_score(const Geom& g, const ScorePlan& sp, int n_layers, const void* q,
+                        const PoolPtrs& k_pools, const int32_t* trig, const int32_t* block_table,
+                        const int32_t* win_start, const int32_t* status, float* partials,
+                        hipStream_t stream);
+hipError_t launch_reduce_splits(const Geom& g, int64_t n_units, int n_splits, const float* partials,
+                                float* scores, hipStream_t stream);
+
+// Selection (kara_select.hip).  mode bit 1: discrete top-k; bit 2: Token2Chunk
+// + fill.  Scores come either from `scores` or, when `partials` is non-null,
+// from the partial column sums (n_splits slabs per unit), in which case the
+// reduced scores are also written to `scores` if it is non-null.
+enum { kSelectDiscrete = 1, kSelectKept = 2 };
+hipError_t launch_select(const Geom& g, int64_t n_units, int mode, const float* partials,
+                         int n_splits, float* scores, const int32_t* discrete_in,
+                         int32_t* discrete_out, int32_t* kept_out, hipStream_t stream);
+
+// Compaction and metadata (kara_pages.hip).
+hipError_t launch_check_kept(const Geom& g, int n_layers, const int32_t* kept, int32_t* status,
+                             hipStream_t stream);
+hipError_t launch_compact(const Geom& g, int n_layers, const int32_t* trig, const int32_t* kept,
+                          const PoolPtrs& k_pools, const PoolPtrs& v_pools,
+                          const int32_t* block_table, const int32_t* seq_lens,
+                          const int32_t* win_start, const int32_t* status, hipStream_t stream);
+hipError_t launch_commit(const Geom& g, const int32_t* trig, int32_t* block_table,
+                         int32_t* seq_lens, const int32_t* win_start, int32_t* freed,
+                         int32_t* n_freed, const int32_t* status, hipStream_t stream);
+
+}  // namespace kara

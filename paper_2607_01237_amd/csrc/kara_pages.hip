@@ -1,0 +1,190 @@
+// Paged-cache side of the step: window validation, the in-place window gather
+// of Eq. (9) (Algorithm 1's MemoryCompaction) and the metadata update
+// (UpdateMetadata: trailing blocks released, table and length rewritten).
+#include "kara_internal.h"
+
+namespace kara {
+namespace {
+
+__global__ void validate_kernel(Geom g, const int32_t* __restrict__ trig,
+                                const int32_t* __restrict__ bt, const int32_t* __restrict__ seq_lens,
+                                const int32_t* __restrict__ win_start, int32_t* __restrict__ status) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= g.n_trig) return;
+  const int s = trig[t];
+  if (s < 0 || s >= g.n_seqs) {
+    status[t] = KARA_SEQ_BAD_INDEX;
+    return;
+  }
+  int st = 0;
+  for (int o = 0; o < g.n_trig; ++o)
+    if (o != t && trig[o] == s) {
+      st |= KARA_SEQ_DUP_TRIGGER;
+      break;
+    }
+  const int p0 = win_start[s];
+  const int len = seq_lens[s];
+  if (p0 < 0 || (int64_t)p0 + g.W > (int64_t)len || (int64_t)len > (int64_t)g.max_blocks * g.bs) {
+    status[t] = st | KARA_SEQ_BAD_WINDOW;
+    return;
+  }
+  const int32_t* row = bt + (int64_t)s * g.max_blocks;
+  const int b1 = (len + g.bs - 1) / g.bs;
+  for (int b = p0 / g.bs; b < b1; ++b) {
+    const int pg = row[b];
+    if (pg < 0 || pg >= g.num_pages) {
+      st |= KARA_SEQ_BAD_PAGE;
+      break;
+    }
+  }
+  status[t] = st;
+}
+
+// Flags triggered sequences whose kept rows (caller-supplied) are not a
+// strictly ascending subset of [0, N); one workgroup per unit.
+__global__ void check_kept_kernel(Geom g, int n_layers, const int32_t* __restrict__ kept,
+                                  int32_t* __restrict__ status) {
+  const int64_t u = blockIdx.x;
+  const int t = (int)((u / g.Hkv) % g.n_trig);
+  const int32_t* kr = kept + u * g.budget;
+  int bad = 0;
+  for (int j = threadIdx.x; j < g.budget; j += blockDim.x) {
+    const int v = kr[j];
+    if (v < 0 || v >= g.N || (j > 0 && kr[j - 1] >= v)) bad = 1;
+  }
+  if (__syncthreads_or(bad) && threadIdx.x == 0) atomicOr(&status[t], KARA_SEQ_BAD_KEPT);
+}
+
+constexpr int kCompactThreads = 256;
+constexpr int kCompactUnroll = 4;
+
+// One workgroup per (unit, K|V).  Destination row j (window-relative) takes
+// source row m(j): kept[j] for j < budget, then the buffer rows W-U.., then
+// the tail rows W..  m is strictly increasing with m(j) >= j, so processing
+// destination tiles in ascending order -- every source of a tile loaded
+// before any row of it is stored -- never overwrites a row still to be read.
+__global__ __launch_bounds__(kCompactThreads) void compact_kernel(
+    Geom g, const int32_t* __restrict__ trig, const int32_t* __restrict__ kept, PoolPtrs kp,
+    PoolPtrs vp, const int32_t* __restrict__ bt, const int32_t* __restrict__ seq_lens,
+    const int32_t* __restrict__ win_start, const int32_t* __restrict__ status) {
+  const int64_t bid = blockIdx.x;
+  const int kv = (int)(bid & 1);
+  const int64_t u = bid >> 1;
+  const int h = (int)(u % g.Hkv);
+  const int t = (int)((u / g.Hkv) % g.n_trig);
+  const int l = (int)(u / ((int64_t)g.Hkv * g.n_trig));
+  if (status[t] != 0) return;
+  const int s = trig[t];
+  const int p0 = win_start[s];
+  const int tail = seq_lens[s] - p0 - g.W;
+  const int n_dst = g.budget + g.U + tail;
+  const int32_t* __restrict__ kr = kept + u * g.budget;
+  char* base = (char*)(kv ? vp.p[l] : kp.p[l]);
+  const int32_t* __restrict__ row_pages = bt + (int64_t)s * g.max_blocks;
+  const int row_bytes = g.d * g.esize;
+  const int cpr = row_bytes >> 4;          // 16-byte chunks per row
+  const int rpp = kCompactThreads / cpr;   // rows per pass
+  const int tile = rpp * kCompactUnroll;
+  const int c = threadIdx.x % cpr;
+  const int r = threadIdx.x / cpr;
+
+  auto row_addr = [&](int x) -> char* {
+    const int pos = p0 + x;
+    const int64_t page = row_pages[pos / g.bs];
+    return base + ((page * g.Hkv + h) * g.bs + pos % g.bs) * (int64_t)row_bytes + c * 16;
+  };
+
+  for (int x0 = 0; x0 < n_dst; x0 += tile) {
+    uint4 v[kCompactUnroll];
+    int dst[kCompactUnroll];
+#pragma unroll
+    for (int k = 0; k < kCompactUnroll; ++k) {
+      const int j = x0 + k * rpp + r;
+      dst[k] = -1;
+      if (j < n_dst) {
+        const int src = j < g.budget ? kr[j]
+                                     : (j < g.budget + g.U ? g.N + (j - g.budget) : g.W + (j - g.budget - g.U));
+        if (src != j) {
+          dst[k] = j;
+          v[k] = *(const uint4*)row_addr(src);
+        }
+      }
+    }
+    // all of this tile's loads have landed before any thread stores
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kCompactUnroll; ++k)
+      if (dst[k] >= 0) *(uint4*)row_addr(dst[k]) = v[k];
+  }
+}
+
+__global__ void commit_kernel(Geom g, const int32_t* __restrict__ trig, int32_t* __restrict__ bt,
+                              int32_t* __restrict__ seq_lens, int32_t* __restrict__ freed,
+                              int32_t* __restrict__ n_freed, const int32_t* __restrict__ status) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= g.n_trig) return;
+  int32_t* fr = freed + (int64_t)t * g.max_blocks;
+  if (status[t] != 0) {
+    n_freed[t] = 0;
+    for (int b = 0; b < g.max_blocks; ++b) fr[b] = -1;
+    return;
+  }
+  const int s = trig[t];
+  const int len = seq_lens[s];
+  const int new_len = len - (g.N - g.budget);
+  const int old_b = (len + g.bs - 1) / g.bs;
+  const int new_b = (new_len + g.bs - 1) / g.bs;
+  int32_t* row = bt + (int64_t)s * g.max_blocks;
+  int c = 0;
+  for (int b = new_b; b < old_b; ++b) {
+    fr[c++] = row[b];
+    row[b] = -1;
+  }
+  for (; c < g.max_blocks; ++c) fr[c] = -1;
+  n_freed[t] = old_b - new_b;
+  seq_lens[s] = new_len;
+}
+
+}  // namespace
+
+hipError_t launch_validate(const Geom& g, const int32_t* trig, const int32_t* block_table,
+                           const int32_t* seq_lens, const int32_t* win_start, int32_t* status,
+                           hipStream_t stream) {
+  const int threads = 256;
+  const int blocks = (g.n_trig + threads - 1) / threads;
+  hipLaunchKernelGGL(validate_kernel, dim3(blocks), dim3(threads), 0, stream, g, trig, block_table,
+                     seq_lens, win_start, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_check_kept(const Geom& g, int n_layers, const int32_t* kept, int32_t* status,
+                             hipStream_t stream) {
+  const int64_t units = (int64_t)n_layers * g.n_trig * g.Hkv;
+  hipLaunchKernelGGL(check_kept_kernel, dim3((unsigned)units), dim3(256), 0, stream, g, n_layers,
+                     kept, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_compact(const Geom& g, int n_layers, const int32_t* trig, const int32_t* kept,
+                          const PoolPtrs& k_pools, const PoolPtrs& v_pools,
+                          const int32_t* block_table, const int32_t* seq_lens,
+                          const int32_t* win_start, const int32_t* status, hipStream_t stream) {
+  const int64_t units = (int64_t)n_layers * g.n_trig * g.Hkv;
+  hipLaunchKernelGGL(compact_kernel, dim3((unsigned)(units * 2)), dim3(kCompactThreads), 0, stream, g,
+                     trig, kept, k_pools, v_pools, block_table, seq_lens, win_start, status);
+  return hipGetLastError();
+}
+
+hipError_t launch_commit(const Geom& g, const int32_t* trig, int32_t* block_table,
+                         int32_t* seq_lens, const int32_t* win_start, int32_t* freed,
+                         int32_t* n_freed, const int32_t* status, hipStream_t stream) {
+  (void)win_start;
+  const int threads = 256;
+  const int blocks = (g.n_trig + threads - 1) / threads;
+  hipLaunchKernelGGL(commit_kernel, dim3(blocks), dim3(threads), 0, stream, g, trig, block_table,
+                     seq_lens, freed, n_freed, status);
+  return hipGetLastError();
+}
+
+}  // namespace kara

@@ -1,0 +1,307 @@
+// Per-unit selection on chip: discrete TopK (Eq. (5)), Token2Chunk
+// (Eq. (6)-(8)) and the fill rule of App. C.3.  One workgroup per
+// (sequence, layer, KV head); the unit's scores live in LDS, every ranking is
+// an exact block-wide radix select on order-preserving integer keys with
+// ties resolved by position, so the result is deterministic and independent
+// of thread scheduling.
+#include "kara_internal.h"
+
+namespace kara {
+namespace {
+
+constexpr int kSelThreads = 256;
+constexpr int kSelEpt = KARA_MAX_COMPRESSIBLE / kSelThreads;  // positions per thread
+constexpr int kSelWaves = kSelThreads / 64;
+
+struct SelSmem {
+  float a[KARA_MAX_COMPRESSIBLE];
+  int32_t disc[KARA_MAX_COMPRESSIBLE];
+  uint8_t mark[KARA_MAX_COMPRESSIBLE];  // bit0 discrete, bit1 chunk interior, bit2 fill
+  uint32_t hist[256];
+  uint32_t wsum[kSelWaves];
+  uint32_t bc[2];
+};
+
+// Order-preserving maps to unsigned keys (larger value -> larger key); -0
+// ranks equal to +0, as in a floating-point comparison.
+__device__ inline uint32_t ord32(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) == 0) u = 0;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ inline uint64_t ord64(double x) {
+  uint64_t u = (uint64_t)__double_as_longlong(x);
+  if ((u & 0x7fffffffffffffffull) == 0) u = 0;
+  return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+
+// Eq. (6): chunk score from the fp32 endpoint scores, in fp64 (the sum of two
+// fp32 values and its product with a small integer round the same way on
+// every IEEE implementation; no contraction).
+__device__ inline double chunk_score(float a_lo, float a_hi, int gap) {
+#pragma clang fp contract(off)
+  const double s = (double)a_lo + (double)a_hi;
+  return s * (double)(gap - 1);
+}
+
+__device__ inline uint32_t wave_incl_scan(uint32_t v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t n = __shfl_up(v, o, 64);
+    if (lane >= o) v += n;
+  }
+  return v;
+}
+
+// Exclusive prefix sum over threads in index order; *total = block sum.
+__device__ uint32_t block_excl_scan(uint32_t v, SelSmem& sm, uint32_t* total) {
+  const uint32_t inc = wave_incl_scan(v);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 63) sm.wsum[w] = inc;
+  __syncthreads();
+  uint32_t off = 0, tot = 0;
+#pragma unroll
+  for (int i = 0; i < kSelWaves; ++i) {
+    const uint32_t x = sm.wsum[i];
+    off += (i < w) ? x : 0u;
+    tot += x;
+  }
+  __syncthreads();
+  *total = tot;
+  return off + inc - v;
+}
+
+// Marks in sel[] the K best eligible items -- larger key first, lower
+// position first among equal keys -- where thread i owns positions
+// [i*ept, i*ept+ept).  MSB-first radix select over 8-bit digits finds the
+// K-th key; items equal to it are then taken in position order.
+template <typename KeyT>
+__device__ void select_top(const KeyT (&key)[kSelEpt], const bool (&elig)[kSelEpt],
+                           bool (&sel)[kSelEpt], uint32_t K, SelSmem& sm) {
+  constexpr int kBits = sizeof(KeyT) * 8;
+  uint32_t cnt = 0;
+#pragma unroll
+  for (int e = 0; e < kSelEpt; ++e) cnt += elig[e] ? 1u : 0u;
+  uint32_t n_el;
+  block_excl_scan(cnt, sm, &n_el);
+  if (K >= n_el || K == 0) {
+#pragma unroll
+    for (int e = 0; e < kSelEpt; ++e) sel[e] = K != 0 && elig[e];
+    return;
+  }
+  KeyT prefix = 0;
+  uint32_t remaining = K;
+  for (int shift = kBits - 8; shift >= 0; shift -= 8) {
+    sm.hist[threadIdx.x] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < kSelEpt; ++e) {
+      if (!elig[e]) continue;
+      const bool match = (shift == kBits - 8) || (((key[e] ^ prefix) >> (shift + 8)) == 0);
+      if (match) atomicAdd(&sm.hist[(uint32_t)(key[e] >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    const uint32_t b = 255u - threadIdx.x;   // thread i looks at bin 255-i
+    const uint32_t h = sm.hist[b];
+    uint32_t tot;
+    const uint32_t above = block_excl_scan(h, sm, &tot);   // items in bins > b
+    if (above < remaining && above + h >= remaining) {
+      sm.bc[0] = b;
+      sm.bc[1] = remaining - above;
+    }
+    __syncthreads();
+    prefix |= (KeyT)sm.bc[0] << shift;
+    remaining = sm.bc[1];
+    __syncthreads();
+  }
+  uint32_t eq = 0;
+#pragma unroll
+  for (int e = 0; e < kSelEpt; ++e) eq += (elig[e] && key[e] == prefix) ? 1u : 0u;
+  uint32_t tot;
+  uint32_t rank = block_excl_scan(eq, sm, &tot);
+#pragma unroll
+  for (int e = 0; e < kSelEpt; ++e) {
+    const bool is_eq = elig[e] && key[e] == prefix;
+    sel[e] = (elig[e] && key[e] > prefix) || (is_eq && rank < remaining);
+    rank += is_eq ? 1u : 0u;
+  }
+}
+
+__global__ __launch_bounds__(kSelThreads) void select_kernel(
+    Geom g, int mode, const float* __restrict__ partials, int n_splits, float* __restrict__ scores,
+    const int32_t* __restrict__ disc_in, int32_t* __restrict__ disc_out,
+    int32_t* __restrict__ kept_out) {
+  __shared__ SelSmem sm;
+  const int64_t u = blockIdx.x;
+  const int N = g.N;
+  const int tid = threadIdx.x;
+  const int k = g.k_disc;
+
+  // Scores of the unit: the fixed-order sum of the partial column sums, or
+  // the caller's scores.
+  for (int j = tid; j < N; j += kSelThreads) {
+    float v;
+    if (partials) {
+      const float* pp = partials + u * n_splits * (int64_t)N + j;
+      v = pp[0];
+      for (int s = 1; s < n_splits; ++s) v += pp[(int64_t)s * N];
+      if (scores) scores[u * N + j] = v;
+    } else {
+      v = scores[u * N + j];
+    }
+    sm.a[j] = v;
+    sm.mark[j] = 0;
+  }
+  __syncthreads();
+
+  const int ept = (N + kSelThreads - 1) / kSelThreads;
+  const int base = tid * ept;
+  uint32_t key[kSelEpt];
+  bool elig[kSelEpt], sel[kSelEpt];
+
+  if (mode & kSelectDiscrete) {
+    // Eq. (5): the budget - alpha best positions, kept ascending
+#pragma unroll
+    for (int e = 0; e < kSelEpt; ++e) {
+      const int j = base + e;
+      elig[e] = e < ept && j < N;
+      key[e] = elig[e] ? ord32(sm.a[j]) : 0u;
+    }
+    select_top(key, elig, sel, (uint32_t)k, sm);
+    uint32_t c = 0;
+#pragma unroll
+    for (int e = 0; e < kSelEpt; ++e) c += sel[e] ? 1u : 0u;
+    uint32_t tot;
+    uint32_t r = block_excl_scan(c, sm, &tot);
+#pragma unroll
+    for (int e = 0; e < kSelEpt; ++e)
+      if (sel[e]) {
+        const int j = base + e;
+        sm.disc[r] = j;
+        sm.mark[j] = 1;
+        if (disc_out) disc_out[u * k + r] = j;
+        ++r;
+      }
+  } else {
+    int bad = 0;
+    for (int i = tid; i < k; i += kSelThreads) {
+      const int v = disc_in[u * k + i];
+      sm.disc[i] = v;
+      if (v < 0 || v >= N) bad = 1;
+    }
+    __syncthreads();
+    for (int i = tid; i + 1 < k; i += kSelThreads)
+      if (sm.disc[i] >= sm.disc[i + 1]) bad = 1;
+    if (__syncthreads_or(bad)) {
+      for (int i = tid; i < g.budget; i += kSelThreads) kept_out[u * g.budget + i] = -1;
+      return;
+    }
+    for (int i = tid; i < k; i += kSelThreads) sm.mark[sm.disc[i]] = 1;
+  }
+  __syncthreads();
+  if (!(mode & kSelectKept)) return;
+
+  // Eq. (6)-(8): candidate chunk i spans (disc[i], disc[i+1]) when its length
+  // with both endpoints is at most gamma and its interior is not empty; the
+  // n_chunks best (R desc, i asc) add their interiors.
+  uint32_t added_here = 0;
+  if (g.n_chunks > 0 && k >= 2) {
+    const int nc = k - 1;
+    const int ept2 = (nc + kSelThreads - 1) / kSelThreads;
+    const int base2 = tid * ept2;
+    uint64_t key2[kSelEpt];
+    bool el2[kSelEpt], s2[kSelEpt];
+#pragma unroll
+    for (int e = 0; e < kSelEpt; ++e) {
+      const int i = base2 + e;
+      el2[e] = false;
+      key2[e] = 0;
+      if (e < ept2 && i < nc) {
+        const int lo = sm.disc[i], hi = sm.disc[i + 1];
+        const int gap = hi - lo;
+        if (gap >= 2 && gap <= g.gamma - 1) {
+          key2[e] = ord64(chunk_score(sm.a[lo], sm.a[hi], gap));
+          el2[e] = true;
+        }
+      }
+    }
+    select_top(key2, el2, s2, (uint32_t)g.n_chunks, sm);
+#pragma unroll
+    for (int e = 0; e < kSelEpt; ++e)
+      if (s2[e]) {
+        const int i = base2 + e;
+        const int lo = sm.disc[i], hi = sm.disc[i + 1];
+        for (int x = lo + 1; x < hi; ++x) sm.mark[x] |= 2;
+        added_here += (uint32_t)(hi - lo - 1);
+      }
+  }
+  uint32_t added;
+  block_excl_scan(added_here, sm, &added);
+
+  // App. C.3: top up to alpha added positions with the best unselected ones
+  const int fill = g.alpha - (int)added;
+  if (fill > 0) {
+#pragma unroll
+    for (int e = 0; e < kSelEpt; ++e) {
+      const int j = base + e;
+      elig[e] = e < ept && j < N && sm.mark[j] == 0;
+      key[e] = elig[e] ? ord32(sm.a[j]) : 0u;
+    }
+    select_top(key, elig, sel, (uint32_t)fill, sm);
+#pragma unroll
+    for (int e = 0; e < kSelEpt; ++e)
+      if (sel[e]) sm.mark[base + e] |= 4;
+  }
+  __syncthreads();
+
+  // the kept set, ascending
+  uint32_t c = 0;
+#pragma unroll
+  for (int e = 0; e < kSelEpt; ++e) {
+    const int j = base + e;
+    if (e < ept && j < N && sm.mark[j]) ++c;
+  }
+  uint32_t tot;
+  uint32_t r = block_excl_scan(c, sm, &tot);
+#pragma unroll
+  for (int e = 0; e < kSelEpt; ++e) {
+    const int j = base + e;
+    if (e < ept && j < N && sm.mark[j]) kept_out[u * g.budget + r++] = j;
+  }
+}
+
+__global__ void reduce_splits_kernel(int64_t n, int N, int n_splits, const float* __restrict__ partials,
+                                     float* __restrict__ scores) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int64_t u = i / N;
+  const int j = (int)(i % N);
+  const float* pp = partials + u * n_splits * (int64_t)N + j;
+  float v = pp[0];
+  for (int s = 1; s < n_splits; ++s) v += pp[(int64_t)s * N];
+  scores[i] = v;
+}
+
+}  // namespace
+
+hipError_t launch_select(const Geom& g, int64_t n_units, int mode, const float* partials,
+                         int n_splits, float* scores, const int32_t* discrete_in,
+                         int32_t* discrete_out, int32_t* kept_out, hipStream_t stream) {
+  if (n_units <= 0) return hipSuccess;
+  hipLaunchKernelGGL(select_kernel, dim3((unsigned)n_units), dim3(kSelThreads), 0, stream, g, mode,
+                     partials, n_splits, scores, discrete_in, discrete_out, kept_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_splits(const Geom& g, int64_t n_units, int n_splits, const float* partials,
+                                float* scores, hipStream_t stream) {
+  const int64_t n = n_units * g.N;
+  if (n <= 0) return hipSuccess;
+  const int threads = 256;
+  hipLaunchKernelGGL(reduce_splits_kernel, dim3((unsigned)((n + threads - 1) / threads)), dim3(threads), 0,
+                     stream, n, g.N, n_splits, partials, scores);
+  return hipGetLastError();
+}
+
+}  // namespace kara

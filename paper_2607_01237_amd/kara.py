@@ -1,0 +1,191 @@
+"""ctypes binding of libkara (include/kara.h): argument marshalling only.
+
+Every function takes torch tensors that already live on the GPU and passes
+their device pointers, plus the current HIP stream, to the C ABI of the same
+name.  All computation happens in the library's HIP kernels; nothing here
+falls back to the CPU.  A missing or unloadable library raises KaraError.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libkara.so")
+HEADER = os.path.join(os.path.dirname(_PKG), "include", "kara.h")
+
+BF16, F32 = 0, 1
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
+SEQ_OK, SEQ_BAD_WINDOW, SEQ_BAD_PAGE, SEQ_DUP_TRIGGER, SEQ_BAD_INDEX, SEQ_BAD_KEPT = 0, 1, 2, 4, 8, 16
+MAX_COMPRESSIBLE = 4096
+
+
+class KaraError(RuntimeError):
+    def __init__(self, fn, code, msg):
+        super().__init__(f"{fn}: {msg} ({code})")
+        self.code = code
+
+
+class KaraParams(ctypes.Structure):
+    _fields_ = [
+        ("window", ctypes.c_int32),
+        ("buffer", ctypes.c_int32),
+        ("budget", ctypes.c_int32),
+        ("chunk_budget", ctypes.c_int32),
+        ("max_chunk_len", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32),
+        ("block_size", ctypes.c_int32),
+        ("num_pages", ctypes.c_int32),
+        ("max_blocks_per_seq", ctypes.c_int32),
+        ("n_seqs", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("scale", ctypes.c_float),
+    ]
+
+
+def make_params(p: dict, n_seqs: int) -> KaraParams:
+    """KaraParams from a geometry dict (the field names of kara_params_t)."""
+    dt = p["dtype"]
+    dt = BF16 if dt in ("bf16", BF16) else F32 if dt in ("f32", F32) else dt
+    return KaraParams(p["window"], p["buffer"], p["budget"], p["chunk_budget"], p["max_chunk_len"],
+                      p["head_dim"], p["n_q_heads"], p["n_kv_heads"], p["block_size"], p["num_pages"],
+                      p["max_blocks_per_seq"], n_seqs, dt, float(p.get("scale", 0.0) or 0.0))
+
+
+_VP = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_PP = ctypes.POINTER(ctypes.c_void_p)
+_PAR = ctypes.POINTER(KaraParams)
+
+_SIGS = {
+    "kara_status_string": (ctypes.c_char_p, [_I32]),
+    "kara_abi_version": (_I32, []),
+    "kara_workspace_size": (_I32, [_PAR, _I32, _I32, ctypes.POINTER(ctypes.c_size_t)]),
+    "kara_validate": (_I32, [_PAR, _I32, _VP, _VP, _VP, _VP, _VP, _VP]),
+    "kara_score_window": (_I32, [_PAR, _I32, _VP, _I32, _VP, _PP, _VP, _VP, _VP, _VP, _VP, _VP,
+                                 ctypes.c_size_t, _VP]),
+    "kara_select": (_I32, [_PAR, ctypes.c_int64, _VP, _VP, _VP]),
+    "kara_token2chunk": (_I32, [_PAR, ctypes.c_int64, _VP, _VP, _VP, _VP]),
+    "kara_compact_pages": (_I32, [_PAR, _I32, _VP, _I32, _VP, _PP, _PP, _VP, _VP, _VP, _VP, _VP]),
+    "kara_commit_tables": (_I32, [_PAR, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
+    "kara_compress_window": (_I32, [_PAR, _I32, _VP, _I32, _VP, _PP, _PP, _VP, _VP, _VP, _I32, _VP, _VP,
+                                    _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP]),
+}
+
+_lib = None
+
+
+def header_functions() -> list[str]:
+    """Names of the functions include/kara.h declares."""
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\S.*?\b(kara_\w+)\s*\(", text, flags=re.M)))
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise KaraError("load", ERR_HIP, f"{path} is not built; run paper_2607_01237_amd.build")
+    try:
+        lib = ctypes.CDLL(path)
+    except OSError as e:
+        raise KaraError("load", ERR_HIP, f"cannot load {path}: {e}") from e
+    for name, (res, args) in _SIGS.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def status_string(code: int) -> str:
+    return load().kara_status_string(code).decode()
+
+
+def _check(fn: str, code: int):
+    if code != OK:
+        raise KaraError(fn, code, status_string(code))
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise KaraError("marshal", ERR_INVALID_ARG, "tensor is not on the GPU")
+    if not t.is_contiguous():
+        raise KaraError("marshal", ERR_INVALID_ARG, "tensor is not contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _ptr_array(tensors):
+    arr = (ctypes.c_void_p * len(tensors))()
+    for i, t in enumerate(tensors):
+        arr[i] = _ptr(t).value
+    return arr
+
+
+def _stream(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def abi_version() -> int:
+    return int(load().kara_abi_version())
+
+
+def workspace_size(p: KaraParams, n_trig: int, n_layers: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check("kara_workspace_size", load().kara_workspace_size(ctypes.byref(p), n_trig, n_layers, ctypes.byref(out)))
+    return int(out.value)
+
+
+def validate(p, trig, block_table, seq_lens, win_start, status, stream=None):
+    _check("kara_validate", load().kara_validate(ctypes.byref(p), trig.numel(), _ptr(trig), _ptr(block_table),
+                                                 _ptr(seq_lens), _ptr(win_start), _ptr(status), _stream(stream)))
+
+
+def score_window(p, trig, q, k_pools, block_table, seq_lens, win_start, scores, status, workspace,
+                 stream=None):
+    _check("kara_score_window", load().kara_score_window(
+        ctypes.byref(p), trig.numel(), _ptr(trig), len(k_pools), _ptr(q), _ptr_array(k_pools),
+        _ptr(block_table), _ptr(seq_lens), _ptr(win_start), _ptr(scores), _ptr(status),
+        _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def select(p, scores, discrete, stream=None):
+    n_units = scores.numel() // (p.window - p.buffer)
+    _check("kara_select", load().kara_select(ctypes.byref(p), n_units, _ptr(scores), _ptr(discrete),
+                                             _stream(stream)))
+
+
+def token2chunk(p, scores, discrete, kept, stream=None):
+    n_units = scores.numel() // (p.window - p.buffer)
+    _check("kara_token2chunk", load().kara_token2chunk(ctypes.byref(p), n_units, _ptr(scores), _ptr(discrete),
+                                                       _ptr(kept), _stream(stream)))
+
+
+def compact_pages(p, trig, kept, k_pools, v_pools, block_table, seq_lens, win_start, status, stream=None):
+    _check("kara_compact_pages", load().kara_compact_pages(
+        ctypes.byref(p), trig.numel(), _ptr(trig), len(k_pools), _ptr(kept), _ptr_array(k_pools),
+        _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), _ptr(win_start), _ptr(status), _stream(stream)))
+
+
+def commit_tables(p, trig, block_table, seq_lens, win_start, freed, n_freed, status, stream=None):
+    _check("kara_commit_tables", load().kara_commit_tables(
+        ctypes.byref(p), trig.numel(), _ptr(trig), _ptr(block_table), _ptr(seq_lens), _ptr(win_start),
+        _ptr(freed), _ptr(n_freed), _ptr(status), _stream(stream)))
+
+
+def compress_window(p, trig, q, k_pools, v_pools, block_table, seq_lens, win_start, commit, status,
+                    workspace, scores=None, discrete=None, kept=None, freed=None, n_freed=None, stream=None):
+    _check("kara_compress_window", load().kara_compress_window(
+        ctypes.byref(p), trig.numel(), _ptr(trig), len(k_pools), _ptr(q), _ptr_array(k_pools),
+        _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), _ptr(win_start), int(bool(commit)),
+        _ptr(scores), _ptr(discrete), _ptr(kept), _ptr(freed), _ptr(n_freed), _ptr(status), _ptr(workspace),
+        workspace.numel() * workspace.element_size() if workspace is not None else 0, _stream(stream)))

@@ -1,0 +1,267 @@
+"""Test harness: runs libkara on a seeded workload and checks it against the
+CPU oracle (parity procedure P1-P4).
+
+P1  scores within |A_gpu - A_ora| <= 1e-5 + 2e-3 |A_ora| (fp32 accumulation
+    against fp64; the tolerance the step is specified with).
+P2  the oracle's selection run on the GPU's own scores reproduces the GPU's
+    discrete and kept sets bit for bit (same fp32 inputs, same decisions).
+P3  end to end, the GPU's kept sets equal the oracle's, except in units whose
+    oracle decision boundary (k-th score, n_c-th chunk score, fill score) is
+    a near-tie within the score tolerance.
+P4  compaction: the oracle's gather, run with the GPU's kept sets on a host
+    snapshot, equals the GPU's live cache rows bit for bit, and the block
+    tables, lengths and freed-page lists match exactly.
+"""
+
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+import kara_inputs as ki
+import oracle
+from paper_2607_01237_amd import kara
+
+RTOL, ATOL = 2e-3, 1e-5
+
+
+def tol(a):
+    return ATOL + RTOL * np.abs(a)
+
+
+@dataclass
+class Case:
+    geom: ki.Geometry
+    p: dict
+    params: kara.KaraParams
+    q: torch.Tensor
+    kp: list
+    vp: list
+    bt: torch.Tensor
+    seq_lens: torch.Tensor
+    win_start: torch.Tensor
+    trig: torch.Tensor
+    host: dict
+
+
+def setup(cfg: dict, device="cuda", trig=None, seq_lens=None, win_start=None, block_table=None) -> Case:
+    geom = ki.make_geometry(cfg)
+    if trig is not None:
+        geom.trig = np.asarray(trig, dtype=np.int32)
+    if seq_lens is not None:
+        geom.seq_lens = np.asarray(seq_lens, dtype=np.int32)
+    if win_start is not None:
+        geom.win_start = np.asarray(win_start, dtype=np.int32)
+    if block_table is not None:
+        geom.block_table = np.asarray(block_table, dtype=np.int32)
+    p = geom.params()
+    L = cfg["n_layers"]
+    q = torch.stack([ki.make_queries(geom, l, device) for l in range(L)]).contiguous()
+    pools = [ki.make_pools(geom, l, device) for l in range(L)]
+    kp = [x[0] for x in pools]
+    vp = [x[1] for x in pools]
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
+    case = Case(geom=geom, p=p, params=kara.make_params(p, geom.block_table.shape[0]), q=q, kp=kp, vp=vp,
+                bt=dev(geom.block_table), seq_lens=dev(geom.seq_lens), win_start=dev(geom.win_start),
+                trig=dev(geom.trig), host={})
+    case.host = snapshot(case)
+    return case
+
+
+def snapshot(case: Case) -> dict:
+    return dict(q=ki.raw_numpy(case.q), kp=[ki.raw_numpy(t) for t in case.kp], vp=[ki.raw_numpy(t) for t in case.vp],
+                bt=case.bt.cpu().numpy().copy(), seq_lens=case.seq_lens.cpu().numpy().copy(),
+                win_start=case.win_start.cpu().numpy().copy(), trig=case.trig.cpu().numpy().copy())
+
+
+def n_units(case: Case) -> int:
+    return len(case.kp) * case.trig.numel() * case.p["n_kv_heads"]
+
+
+def run_compress(case: Case, commit=True):
+    """One kara_compress_window call; returns host copies of every output."""
+    p, dev = case.p, case.q.device
+    L, nt, H = len(case.kp), case.trig.numel(), p["n_kv_heads"]
+    N = p["window"] - p["buffer"]
+    ws = torch.empty(kara.workspace_size(case.params, nt, L), dtype=torch.uint8, device=dev)
+    out = dict(
+        scores=torch.full((L, nt, H, N), float("nan"), dtype=torch.float32, device=dev),
+        discrete=torch.full((L, nt, H, p["budget"] - p["chunk_budget"]), -7, dtype=torch.int32, device=dev),
+        kept=torch.full((L, nt, H, p["budget"]), -7, dtype=torch.int32, device=dev),
+        freed=torch.full((nt, p["max_blocks_per_seq"]), -7, dtype=torch.int32, device=dev),
+        n_freed=torch.full((nt,), -7, dtype=torch.int32, device=dev),
+        status=torch.full((nt,), -7, dtype=torch.int32, device=dev),
+    )
+    kara.compress_window(case.params, case.trig, case.q, case.kp, case.vp, case.bt, case.seq_lens, case.win_start,
+                         commit, out["status"], ws, scores=out["scores"], discrete=out["discrete"], kept=out["kept"],
+                         freed=out["freed"], n_freed=out["n_freed"])
+    torch.cuda.synchronize()
+    res = {k: v.cpu().numpy() for k, v in out.items()}
+    res["bt"] = case.bt.cpu().numpy()
+    res["seq_lens"] = case.seq_lens.cpu().numpy()
+    return res
+
+
+# ------------------------------------------------------------------ checks
+def oracle_scores(case: Case, units=None, threads=8):
+    """fp32-rounded oracle scores [L, nt, H, N] (NaN where not computed)."""
+    h = case.host
+    p = case.p
+    L, nt, H = len(h["kp"]), len(h["trig"]), p["n_kv_heads"]
+    N = p["window"] - p["buffer"]
+    st = oracle.validate(p, h["trig"], h["bt"], h["seq_lens"], h["win_start"])
+    if units is None:
+        units = [(l, t, hh) for l in range(L) for t in range(nt) for hh in range(H)]
+    out = np.full((L, nt, H, N), np.nan, dtype=np.float32)
+    ok = [u for u in units if st[u[1]] == 0]
+    for u, a in zip(ok, oracle.score_units(p, h["trig"], h["q"], h["kp"], h["bt"], h["win_start"], ok, threads)):
+        out[u] = oracle.round_scores(a)
+    for u in units:
+        if st[u[1]] != 0:
+            out[u] = 0.0
+    return out, st
+
+
+def check_p1(gpu_scores, ora_scores):
+    m = ~np.isnan(ora_scores)
+    err = np.abs(gpu_scores[m].astype(np.float64) - ora_scores[m].astype(np.float64))
+    bad = err > tol(ora_scores[m].astype(np.float64))
+    assert not bad.any(), f"P1: {bad.sum()} scores out of tolerance, max err {err.max():.3e}"
+    rel = err / np.maximum(np.abs(ora_scores[m]), 1e-30)
+    return dict(max_abs=float(err.max()) if err.size else 0.0, max_rel=float(rel.max()) if rel.size else 0.0,
+                checked=int(m.sum()))
+
+
+def check_p2(p, gpu):
+    """Oracle selection on the GPU's scores == the GPU's index sets."""
+    L, nt, H, _ = gpu["scores"].shape
+    for l in range(L):
+        for t in range(nt):
+            for h in range(H):
+                d, k = oracle.kept_set(gpu["scores"][l, t, h], p["budget"], p["chunk_budget"], p["max_chunk_len"])
+                assert np.array_equal(d, gpu["discrete"][l, t, h]), f"P2 discrete mismatch at unit {(l, t, h)}"
+                assert np.array_equal(k, gpu["kept"][l, t, h]), f"P2 kept mismatch at unit {(l, t, h)}"
+
+
+def _boundary_gaps(a32, p):
+    """Relative margins of the oracle's three decisions for one unit."""
+    budget, alpha, gamma = p["budget"], p["chunk_budget"], p["max_chunk_len"]
+    a = a32.astype(np.float64)
+    order = oracle.rank_order(a32)
+    k = budget - alpha
+    gaps = []
+    if 0 < k < len(a):
+        x, y = a[order[k - 1]], a[order[k]]
+        gaps.append(abs(x - y) <= tol(x) + tol(y))
+    disc = np.sort(order[:k])
+    cands = oracle.chunk_candidates(a32, disc, gamma)
+    nc = alpha // (gamma - 2)
+    if cands and 0 < nc < len(cands):
+        rs = sorted((r for r, _ in cands), reverse=True)
+        # R = (a_i + a_j)(gap-1): tolerance propagates through both endpoints
+        x, y = rs[nc - 1], rs[nc]
+        gaps.append(abs(x - y) <= (gamma - 2) * 4 * (ATOL + RTOL * max(abs(x), abs(y))))
+    _, added = oracle.token2chunk(a32, disc, alpha, gamma)
+    f = alpha - len(added)
+    taken = np.zeros(len(a), bool)
+    taken[disc] = True
+    taken[added] = True
+    free = oracle.rank_order(a32, np.flatnonzero(~taken))
+    if 0 < f < len(free):
+        x, y = a[free[f - 1]], a[free[f]]
+        gaps.append(abs(x - y) <= tol(x) + tol(y))
+    # a changed discrete set also moves the chunk and fill boundaries
+    return any(gaps)
+
+
+def check_p3(p, gpu, ora_scores):
+    L, nt, H, _ = gpu["scores"].shape
+    differ = 0
+    for l in range(L):
+        for t in range(nt):
+            for h in range(H):
+                a = ora_scores[l, t, h]
+                if np.isnan(a).any():
+                    continue
+                _, k = oracle.kept_set(a, p["budget"], p["chunk_budget"], p["max_chunk_len"])
+                if not np.array_equal(k, gpu["kept"][l, t, h]):
+                    differ += 1
+                    assert _boundary_gaps(a, p), f"P3: unit {(l, t, h)} differs without a near-tie"
+    return differ
+
+
+def live_rows(pools, bt, seq_lens, trig_or_all, p):
+    """Every live row (position < seq_len) of the listed sequences, per layer."""
+    bs = p["block_size"]
+    out = []
+    for pool in pools:
+        rows = []
+        for s in trig_or_all:
+            pos = np.arange(int(seq_lens[s]))
+            rows.append(oracle.read_rows(pool, bt[s], pos, slice(None), bs) if len(pos) else
+                        np.zeros((0,) + pool.shape[1:2] + pool.shape[3:], pool.dtype))
+        out.append(rows)
+    return out
+
+
+def gpu_live_rows(t_pool, bt, seq_lens, seqs, p):
+    bs = p["block_size"]
+    pages, slots = [], []
+    for s in seqs:
+        pos = np.arange(int(seq_lens[s]))
+        pages.append(bt[s, pos // bs])
+        slots.append(pos % bs)
+    pg = torch.from_numpy(np.concatenate(pages).astype(np.int64)).to(t_pool.device)
+    sl = torch.from_numpy(np.concatenate(slots).astype(np.int64)).to(t_pool.device)
+    rows = t_pool[pg, :, sl, :]
+    return ki.raw_numpy(rows)
+
+
+def check_p4(case: Case, gpu, commit=True):
+    """Oracle compaction with the GPU's kept sets on the host snapshot."""
+    h = case.host
+    p = case.p
+    kp = [x.copy() for x in h["kp"]]
+    vp = [x.copy() for x in h["vp"]]
+    bt = h["bt"].copy()
+    sl = h["seq_lens"].copy()
+    ora = oracle.compress(p, h["trig"], h["q"], kp, vp, bt, sl, h["win_start"], commit=commit,
+                          score_override=gpu["scores"])
+    assert np.array_equal(ora["status"], gpu["status"]), "P4: status differs"
+    assert np.array_equal(ora["kept"], gpu["kept"]), "P4: kept differs (P2 should have caught this)"
+    assert np.array_equal(bt, gpu["bt"]), "P4: block table differs"
+    assert np.array_equal(sl, gpu["seq_lens"]), "P4: seq_lens differ"
+    if commit:
+        assert np.array_equal(ora["n_freed"], gpu["n_freed"]), "P4: n_freed differs"
+        for t, fr in enumerate(ora["freed"]):
+            want = np.full(p["max_blocks_per_seq"], -1, dtype=np.int32)
+            want[:len(fr)] = fr
+            assert np.array_equal(want, gpu["freed"][t]), f"P4: freed list of trigger {t} differs"
+    seqs = list(range(bt.shape[0]))
+    seqs = [s for s in seqs if sl[s] > 0]
+    for l in range(len(kp)):
+        for name, opools, tpools in (("K", kp, case.kp), ("V", vp, case.vp)):
+            want = np.concatenate([oracle.read_rows(opools[l], bt[s], np.arange(sl[s]), slice(None), p["block_size"])
+                                   for s in seqs])
+            got = gpu_live_rows(tpools[l], bt, sl, seqs, p)
+            assert want.shape == got.shape
+            if not np.array_equal(want.view(np.uint8), got.view(np.uint8)):
+                bad = np.argwhere(np.any(want != got, axis=tuple(range(1, want.ndim))))
+                raise AssertionError(f"P4: {name} layer {l}: {len(bad)} live rows differ (first {bad[:3].ravel()})")
+    return ora
+
+
+def full_check(case: Case, commit=True, units=None):
+    """Runs the fused step and P1-P4; returns a small report."""
+    ora_scores, st = oracle_scores(case, units)
+    gpu = run_compress(case, commit=commit)
+    assert np.array_equal(st, gpu["status"]), f"status {gpu['status']} != oracle {st}"
+    rep = check_p1(gpu["scores"], ora_scores)
+    check_p2(case.p, gpu)
+    rep["p3_units_differing"] = check_p3(case.p, gpu, ora_scores)
+    check_p4(case, gpu, commit)
+    rep["units"] = n_units(case)
+    return rep, gpu

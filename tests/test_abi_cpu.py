@@ -1,0 +1,105 @@
+"""The C-ABI library without a GPU: it loads, exports every function
+include/kara.h declares, and its host-side argument checks reject bad calls
+before anything is launched."""
+import ctypes
+import os
+
+import pytest
+
+from paper_2607_01237_amd import kara
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(kara.LIB_PATH):
+        from paper_2607_01237_amd import build
+        build.build()
+    return kara.load()
+
+
+def good_params(**kw):
+    p = dict(window=1024, buffer=0, budget=205, chunk_budget=16, max_chunk_len=8, head_dim=128,
+             n_q_heads=32, n_kv_heads=8, block_size=16, num_pages=4096, max_blocks_per_seq=200,
+             dtype="bf16", scale=0.0)
+    p.update(kw)
+    return kara.make_params(p, n_seqs=8)
+
+
+def test_exports_every_declared_function(lib):
+    names = kara.header_functions()
+    assert len(names) == 10
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_status_strings(lib):
+    assert kara.abi_version() == 1
+    for code in (0, -1, -2, -3, -4):
+        assert kara.status_string(code).startswith("KARA_")
+    assert "unknown" in kara.status_string(12345)
+
+
+def test_workspace_size_scales(lib):
+    a = kara.workspace_size(good_params(), 8, 1)
+    b = kara.workspace_size(good_params(), 8, 2)
+    assert a > 0 and b > a
+    # at least the scores, index sets and one partial slab per unit
+    units = 8 * 8
+    assert a >= units * (1024 * 4 * 2 + 189 * 4 + 205 * 4)
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("window", 0, kara.ERR_INVALID_ARG),
+    ("buffer", 1024, kara.ERR_INVALID_ARG),
+    ("buffer", -1, kara.ERR_INVALID_ARG),
+    ("budget", 0, kara.ERR_INVALID_ARG),
+    ("budget", 1025, kara.ERR_INVALID_ARG),
+    ("chunk_budget", 205, kara.ERR_INVALID_ARG),
+    ("chunk_budget", -1, kara.ERR_INVALID_ARG),
+    ("max_chunk_len", 2, kara.ERR_INVALID_ARG),
+    ("n_q_heads", 30, kara.ERR_INVALID_ARG),
+    ("head_dim", 96, kara.ERR_UNSUPPORTED),
+    ("dtype", 7, kara.ERR_INVALID_ARG),
+    ("block_size", 0, kara.ERR_INVALID_ARG),
+    ("scale", float("inf"), kara.ERR_INVALID_ARG),
+])
+def test_bad_params_rejected(lib, field, value, code):
+    p = good_params()
+    setattr(p, field, value)
+    out = ctypes.c_size_t(0)
+    assert lib.kara_workspace_size(ctypes.byref(p), 8, 1, ctypes.byref(out)) == code
+
+
+def test_compressible_limit(lib):
+    p = good_params(window=kara.MAX_COMPRESSIBLE + 1, budget=10, chunk_budget=4)
+    out = ctypes.c_size_t(0)
+    assert lib.kara_workspace_size(ctypes.byref(p), 1, 1, ctypes.byref(out)) == kara.ERR_UNSUPPORTED
+    p = good_params(window=kara.MAX_COMPRESSIBLE + 1, buffer=1, budget=10, chunk_budget=4)
+    assert lib.kara_workspace_size(ctypes.byref(p), 1, 1, ctypes.byref(out)) == kara.OK
+
+
+def test_null_pointers_rejected_before_launch(lib):
+    p = good_params()
+    r = ctypes.byref(p)
+    assert lib.kara_validate(r, 4, None, None, None, None, None, None) == kara.ERR_INVALID_ARG
+    assert lib.kara_select(r, 4, None, None, None) == kara.ERR_INVALID_ARG
+    assert lib.kara_token2chunk(r, 4, None, None, None, None) == kara.ERR_INVALID_ARG
+    assert lib.kara_commit_tables(r, 4, None, None, None, None, None, None, None, None) == kara.ERR_INVALID_ARG
+    assert lib.kara_compact_pages(r, 4, None, 1, None, None, None, None, None, None, None, None) == kara.ERR_INVALID_ARG
+    assert lib.kara_score_window(r, 4, None, 1, None, None, None, None, None, None, None, None, 0, None) == kara.ERR_INVALID_ARG
+    assert lib.kara_compress_window(r, 4, None, 1, None, None, None, None, None, None, 1, None, None, None, None,
+                                    None, None, None, 0, None) == kara.ERR_INVALID_ARG
+    # nothing to do is not an error
+    assert lib.kara_select(r, 0, None, None, None) == kara.OK
+    assert lib.kara_validate(r, 0, None, None, None, None, None, None) == kara.OK
+
+
+def test_workspace_checked_before_launch(lib):
+    p = good_params()
+    fake = ctypes.c_void_p(0x1000)   # never dereferenced: the size check fails first
+    pools = (ctypes.c_void_p * 1)(0x1000)
+    rc = lib.kara_compress_window(ctypes.byref(p), 2, fake, 1, fake, pools, pools, fake, fake, fake, 1, None,
+                                  None, None, fake, fake, fake, fake, 16, None)
+    assert rc == kara.ERR_WORKSPACE

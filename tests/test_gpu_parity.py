@@ -1,0 +1,88 @@
+"""GPU parity of the fused step (kara_compress_window) against the CPU oracle,
+on every workload shape at sizes the oracle finishes in seconds, plus the
+edge cases of the method (ragged compressible length, buffer, full budget,
+alpha = 0, gamma = 3, unaligned windows, flagged sequences)."""
+import sys
+
+import numpy as np
+import pytest
+
+import kara_inputs as ki
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _run(cfg, **kw):
+    import kara_check as kc
+    _need_gpu()
+    print(f"\n[case] {cfg['name']} {({k: cfg[k] for k in ('n_seqs', 'n_layers', 'window', 'buffer', 'budget')})}",
+          flush=True)
+    case = kc.setup(cfg, **kw)
+    rep, gpu = kc.full_check(case)
+    print(f"[case] ok {rep}", flush=True)
+    return case, rep, gpu
+
+
+def test_tiny_full():
+    _run(ki.workload("tiny"))
+
+
+def test_batch8_full():
+    _, rep, _ = _run(ki.workload("batch8"))
+    assert rep["units"] == 64
+
+
+def test_qwen14b_shape_reduced():
+    # the 64 x 40-layer batch at its real per-unit shape (W=2048, G=5), fewer units
+    _run(ki.workload("qwen14b", n_seqs=2, n_layers=2, prefix=(4096, 6000)))
+
+
+def test_qwen14b_buffer_ragged_tiles():
+    # U=32: N=2016 is not a multiple of the 16-key tile; budget ceil(0.2*2016)=404
+    _run(ki.workload("qwen14b", n_seqs=2, n_layers=1, buffer=32, budget=404, prefix=(100, 3000)))
+
+
+def test_ragged_reduced():
+    case, rep, gpu = _run(ki.workload("ragged", n_seqs=24, n_layers=2, prefix=(0, 1500)))
+    assert len(case.geom.trig) < 24
+
+
+def test_odd_geometry_and_flags():
+    # N = 193 (ragged), d=64 bf16, block 7, unaligned starts, G=3; one
+    # sequence triggered twice, one with a window past its end
+    cfg = ki.workload("batch8", n_seqs=5, n_layers=2, n_q_heads=6, n_kv_heads=2, head_dim=64, window=200,
+                      buffer=7, budget=39, chunk_budget=5, max_chunk_len=3, block_size=7, num_pages=600,
+                      prefix=(0, 90), tail=(0, 20), key_mode="normal")
+    g = ki.make_geometry(cfg)
+    lens = g.seq_lens.copy()
+    lens[4] = g.win_start[4] + 150          # window overruns the sequence
+    _run(cfg, trig=[0, 1, 2, 3, 4, 2], seq_lens=lens)
+
+
+def test_fp32_head128_mha():
+    cfg = ki.workload("tiny", n_seqs=3, n_q_heads=2, n_kv_heads=2, head_dim=128, window=96, budget=20,
+                      chunk_budget=6, max_chunk_len=5, num_pages=64, prefix=(3, 40), tail=(0, 9))
+    _run(cfg)
+
+
+@pytest.mark.parametrize("budget,alpha,gamma", [(1024, 16, 8), (205, 0, 8), (300, 64, 3), (1, 0, 3)])
+def test_selection_extremes(budget, alpha, gamma):
+    cfg = ki.workload("batch8", n_seqs=2, budget=budget, chunk_budget=alpha, max_chunk_len=gamma)
+    _run(cfg)
+
+
+def test_deterministic():
+    import kara_check as kc
+    _need_gpu()
+    cfg = ki.workload("batch8", n_seqs=3)
+    a = kc.run_compress(kc.setup(cfg))
+    b = kc.run_compress(kc.setup(cfg))
+    for k in ("scores", "discrete", "kept", "bt", "seq_lens", "freed", "n_freed", "status"):
+        assert np.array_equal(a[k].view(np.uint8), b[k].view(np.uint8)), k
