@@ -1,0 +1,306 @@
+"""Benchmark of one Kara compression event on one MI355X.
+
+A step is the whole path -- validation, window scoring, discrete TopK,
+Token2Chunk + fill, in-place compaction of K and V, metadata commit -- for
+every triggered sequence, layer and KV head of one batch, through
+kara_compress_window.  Inputs are resident in HBM before timing starts.
+Between steps only the block table and sequence lengths are restored (a few
+hundred KB, device to device, inside the timed loop); the window's K/V rows
+keep whatever the previous step left, so every step compresses a full
+window of the same shape.
+
+Prints one JSON line.  `value` is window tokens compressed per second
+(triggered sequences x window length per step / step time).  `roofline`
+covers the dominant kernel (scoring) from a staged pass that times each
+stage with HIP events on the launch stream; `roofline_select_compact` covers
+the HBM-bound stages.  `cpu_baseline` times the CPU oracle on a bounded
+sample of units on this host.
+
+    python bench.py [--steps K] [--warmup W] [--workload qwen14b|batch8|ragged|tiny]
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 (matrix and vector)
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="qwen14b")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="rough budget of the CPU-oracle sample")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def setup(cfg, device):
+    import torch
+
+    import kara_inputs as ki
+    from paper_2607_01237_amd import kara
+
+    geom = ki.make_geometry(cfg)
+    p = geom.params()
+    L, nt = cfg["n_layers"], len(geom.trig)
+    dt = ki.torch_dtype(cfg)
+    q = torch.empty((L, nt, cfg["window"], cfg["n_q_heads"], cfg["head_dim"]), dtype=dt, device=device)
+    kp, vp = [], []
+    for l in range(L):
+        q[l] = ki.make_queries(geom, l, device)
+        k_, v_ = ki.make_pools(geom, l, device)
+        kp.append(k_)
+        vp.append(v_)
+        if (l + 1) % 10 == 0:
+            log(f"layer {l + 1}/{L} generated")
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(device)
+    meta = dict(bt=dev(geom.block_table), seq_lens=dev(geom.seq_lens), win_start=dev(geom.win_start),
+                trig=dev(geom.trig))
+    meta["bt0"] = meta["bt"].clone()
+    meta["seq_lens0"] = meta["seq_lens"].clone()
+    params = kara.make_params(p, geom.block_table.shape[0])
+    return geom, p, params, q, kp, vp, meta
+
+
+def moved_rows(kept, p, tails):
+    """Rows that change place in one step (kept rows not already in place plus
+    the buffer and tail rows that shift down), per unit."""
+    budget, W, U = p["budget"], p["window"], p["buffer"]
+    j = np.arange(budget)
+    in_place = (kept == j).sum(axis=-1)                     # [L, nt, H]
+    shift = (W - U) - budget                                # positions the buffer/tail move by
+    extra = (U + tails[None, :, None]) * (1 if shift > 0 else 0)
+    return (budget - in_place) + extra
+
+
+def cpu_baseline(geom, p, host_q, host_k, host_v, budget_s):
+    """The oracle, as it stands, on whole units of the workload."""
+    import oracle
+
+    threads = min(16, len(os.sched_getaffinity(0)))
+    W, U = p["window"], p["buffer"]
+    G = p["n_q_heads"] // p["n_kv_heads"]
+    scale = oracle.scale_of(p)
+    done, t0 = 0, time.perf_counter()
+    from concurrent.futures import ThreadPoolExecutor
+
+    N = W - U
+
+    def one(args):
+        qa, ka, va = args                      # ka, va: window + tail rows
+        a = oracle.round_scores(oracle.window_scores(qa, ka[:N], scale))
+        _, kept = oracle.kept_set(a, p["budget"], p["chunk_budget"], p["max_chunk_len"])
+        oracle.gather_rows(ka, kept, W, U)
+        oracle.gather_rows(va, kept, W, U)
+        return 1
+
+    units = list(host_q.keys())
+    with ThreadPoolExecutor(threads) as ex:
+        for i in range(0, len(units), threads):
+            batch = units[i:i + threads]
+            done += sum(ex.map(one, [(host_q[u], host_k[u], host_v[u]) for u in batch]))
+            if time.perf_counter() - t0 > budget_s:
+                break
+    dt = time.perf_counter() - t0
+    return done, dt, threads
+
+
+def sample_units_host(geom, p, q, kp, vp, n_units_max):
+    """Host fp64 copies of a few units' queries, keys and window+tail values."""
+    import torch
+
+    import kara_inputs as ki
+    import oracle
+
+    H, G, W = p["n_kv_heads"], p["n_q_heads"] // p["n_kv_heads"], p["window"]
+    N = W - p["buffer"]
+    bs = p["block_size"]
+    out_q, out_k, out_v = {}, {}, {}
+    units = [(0, t, h) for t in range(len(geom.trig)) for h in range(H)][:n_units_max]
+    for (l, t, h) in units:
+        s = int(geom.trig[t])
+        p0 = int(geom.win_start[s])
+        rows = q[l, t, :, h * G:(h + 1) * G, :].reshape(W * G, -1)
+        out_q[(l, t, h)] = oracle.to_f64(ki.raw_numpy(rows), p["dtype"])
+        pos = np.arange(p0, int(geom.seq_lens[s]))
+        pg = torch.from_numpy(geom.block_table[s, pos // bs].astype(np.int64)).to(q.device)
+        sl = torch.from_numpy((pos % bs).astype(np.int64)).to(q.device)
+        out_k[(l, t, h)] = oracle.to_f64(ki.raw_numpy(kp[l][pg, h, sl, :]), p["dtype"])
+        out_v[(l, t, h)] = oracle.to_f64(ki.raw_numpy(vp[l][pg, h, sl, :]), p["dtype"])
+    return out_q, out_k, out_v
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 (multi-GPU sharding is "
+                                   "described in DESIGN.md and not built)"}))
+        sys.exit(2)
+    import torch
+
+    import kara_inputs as ki
+    from paper_2607_01237_amd import kara
+
+    kara.load()
+    device = torch.device("cuda:0")
+    torch.cuda.set_device(device)
+    cfg = ki.workload(args.workload)
+    t_setup = time.perf_counter()
+    geom, p, params, q, kp, vp, meta = setup(cfg, device)
+    torch.cuda.synchronize()
+    L, nt, H = cfg["n_layers"], len(geom.trig), p["n_kv_heads"]
+    W, U, N = p["window"], p["buffer"], p["window"] - p["buffer"]
+    G = p["n_q_heads"] // H
+    units = L * nt * H
+    log(f"setup {time.perf_counter() - t_setup:.1f}s: {args.workload} units={units} pages={geom.num_pages} "
+        f"mem={torch.cuda.memory_allocated() / 2**30:.1f} GiB")
+
+    stream = torch.cuda.current_stream()
+    ws = torch.empty(kara.workspace_size(params, nt, L), dtype=torch.uint8, device=device)
+    status = torch.empty(nt, dtype=torch.int32, device=device)
+    freed = torch.empty((nt, p["max_blocks_per_seq"]), dtype=torch.int32, device=device)
+    n_freed = torch.empty(nt, dtype=torch.int32, device=device)
+    scores = torch.empty((L, nt, H, N), dtype=torch.float32, device=device)
+    disc = torch.empty((L, nt, H, p["budget"] - p["chunk_budget"]), dtype=torch.int32, device=device)
+    kept = torch.empty((L, nt, H, p["budget"]), dtype=torch.int32, device=device)
+
+    def restore():
+        meta["bt"].copy_(meta["bt0"], non_blocking=True)
+        meta["seq_lens"].copy_(meta["seq_lens0"], non_blocking=True)
+
+    def step():
+        restore()
+        kara.compress_window(params, meta["trig"], q, kp, vp, meta["bt"], meta["seq_lens"], meta["win_start"], True,
+                             status, ws, kept=kept, freed=freed, n_freed=n_freed, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("warmup done")
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        step()
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = [a.elapsed_time(b) for a, b in ev]
+    st = status.cpu().numpy()
+    assert (st == 0).all(), f"unexpected status {st}"
+    log(f"timed {args.steps} steps: wall {wall * 1e3 / args.steps:.3f} ms/step, events median "
+        f"{np.median(step_ms):.3f} ms")
+
+    # staged pass: the same path through the per-stage entry points, with HIP
+    # events between stages on the launch stream
+    stages = ["score", "select_t2c", "compact", "commit"]
+    times = {s: [] for s in stages}
+    n_stage = max(3, args.steps)
+    for i in range(n_stage + 1):
+        restore()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        e[0].record(stream)
+        kara.score_window(params, meta["trig"], q, kp, meta["bt"], meta["seq_lens"], meta["win_start"], scores,
+                          status, ws, stream=stream)
+        e[1].record(stream)
+        kara.select(params, scores, disc, stream=stream)
+        kara.token2chunk(params, scores, disc, kept, stream=stream)
+        e[2].record(stream)
+        kara.compact_pages(params, meta["trig"], kept, kp, vp, meta["bt"], meta["seq_lens"], meta["win_start"],
+                           status, stream=stream)
+        e[3].record(stream)
+        kara.commit_tables(params, meta["trig"], meta["bt"], meta["seq_lens"], meta["win_start"], freed, n_freed,
+                           status, stream=stream)
+        e[4].record(stream)
+        torch.cuda.synchronize()
+        if i == 0:
+            continue   # first pass warms the staged entry points
+        for k, s in enumerate(stages):
+            times[s].append(e[k].elapsed_time(e[k + 1]))
+    avg = {s: float(np.mean(v)) for s, v in times.items()}
+    log("staged ms: " + ", ".join(f"{s}={avg[s]:.3f}" for s in stages))
+
+    # algorithmic work
+    flops = 2.0 * units * G * W * N * p["head_dim"]
+    peak = PEAK_BF16_TFLOPS if p["dtype"] == "bf16" else PEAK_F32_TFLOPS
+    ach = flops / (avg["score"] * 1e-3) / 1e12
+    es = 2 if p["dtype"] == "bf16" else 4
+    row_bytes = p["head_dim"] * es
+    tails = (geom.seq_lens[geom.trig] - geom.win_start[geom.trig] - W).astype(np.int64)
+    mv = moved_rows(kept.cpu().numpy(), p, tails)
+    compact_bytes = float(mv.sum()) * row_bytes * 2 * 2          # read + write, K and V
+    select_bytes = float(units) * (N * 4 + p["budget"] * 4 + (p["budget"] - p["chunk_budget"]) * 4 * 2)
+    sc_ms = avg["select_t2c"] + avg["compact"]
+    sc_gbs = (compact_bytes + select_bytes) / (sc_ms * 1e-3) / 1e9
+
+    ms = wall * 1e3 / args.steps
+    win_tokens = nt * W
+    result = {
+        "metric": "window tokens compressed/s (score+select+compact); % MFMA peak / % HBM GB/s",
+        "value": win_tokens / (ms * 1e-3),
+        "unit": "window tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "ms_per_step_events_median": float(np.median(step_ms)),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": p["dtype"],
+        "data": "synthetic (seeded N(0,1) Q/K/V of the named shape; no model weights or datasets)",
+        "config": {
+            "workload": args.workload, "sequences": int(nt), "layers": L, "q_heads": p["n_q_heads"],
+            "kv_heads": H, "head_dim": p["head_dim"], "window": W, "buffer": U, "budget": p["budget"],
+            "chunk_budget": p["chunk_budget"], "max_chunk_len": p["max_chunk_len"], "block_size": p["block_size"],
+            "pages": int(geom.num_pages), "units_per_step": int(units),
+        },
+        "roofline": {
+            "kernel": "score_kernel (window scoring, Eq. 4)",
+            "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s", "frac": ach / peak,
+            "traffic": None, "flop_per_launch": flops, "avg_launch_ms": avg["score"],
+        },
+        "roofline_select_compact": {
+            "bound": "hbm", "achieved": sc_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": sc_gbs / PEAK_HBM_GBS,
+            "bytes_per_step": compact_bytes + select_bytes, "avg_ms": sc_ms,
+        },
+        "stage_ms": avg,
+        "layer_window_tokens_per_s": win_tokens * L / (ms * 1e-3),
+    }
+
+    if not args.no_cpu_baseline:
+        n_sample = 16
+        hq, hk, hv = sample_units_host(geom, p, q, kp, vp, n_sample)
+        done, dt_cpu, threads = cpu_baseline(geom, p, hq, hk, hv, args.cpu_seconds)
+        # units per window token: every window token is compressed in L*H units
+        rate = done / dt_cpu * W / (L * H)
+        result["cpu_baseline"] = {
+            "value": rate, "unit": "window tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done} whole units (layer 0, first sequences' KV heads) of this workload: fp64 scoring, "
+                      f"selection, Token2Chunk, fill and K/V gather, {dt_cpu:.1f} s; rate scaled by W/(layers*kv_heads)",
+        }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
