@@ -17,6 +17,8 @@ kara_status_t make_geom(const kara_params_t* p, int32_t n_trig, Geom* g) {
   if (W < 1 || W > kMaxWindow || U < 0 || U >= W) return KARA_ERR_INVALID_ARG;
   const int N = W - U;
   if (N > KARA_MAX_COMPRESSIBLE) return KARA_ERR_UNSUPPORTED;
+  // fp32 windows: at most 64K head-dim elements of keys (1024 keys at d=64, 512 at d=128)
+  if (p->dtype == KARA_F32 && (int64_t)N * p->head_dim > 65536) return KARA_ERR_UNSUPPORTED;
   if (p->budget < 1 || p->budget > N) return KARA_ERR_INVALID_ARG;
   if (p->chunk_budget < 0 || p->chunk_budget >= p->budget) return KARA_ERR_INVALID_ARG;
   if (p->max_chunk_len < 3) return KARA_ERR_INVALID_ARG;
@@ -29,6 +31,10 @@ kara_status_t make_geom(const kara_params_t* p, int32_t n_trig, Geom* g) {
   if (p->dtype != KARA_BF16 && p->dtype != KARA_F32) return KARA_ERR_INVALID_ARG;
   if (std::isinf(p->scale)) return KARA_ERR_INVALID_ARG;
   if (p->head_dim != 64 && p->head_dim != 128) return KARA_ERR_UNSUPPORTED;
+  // the scoring kernel addresses key rows by 32-bit offsets in 16-byte units
+  if ((int64_t)p->num_pages * p->n_kv_heads * p->block_size * p->head_dim *
+          (p->dtype == KARA_BF16 ? 2 : 4) / 16 > (int64_t)UINT32_MAX)
+    return KARA_ERR_UNSUPPORTED;
   g->W = W;
   g->U = U;
   g->N = N;
@@ -55,7 +61,7 @@ kara_status_t make_geom(const kara_params_t* p, int32_t n_trig, Geom* g) {
 inline size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct WsLayout {
-  size_t partials, scores, discrete, kept, total;
+  size_t partials, done, scores, discrete, kept, total;
 };
 
 WsLayout ws_layout(const Geom& g, int n_layers, const ScorePlan& sp) {
@@ -63,7 +69,9 @@ WsLayout ws_layout(const Geom& g, int n_layers, const ScorePlan& sp) {
   WsLayout w{};
   size_t off = 0;
   w.partials = off;
-  off = align_up(off + (size_t)units * sp.n_splits * g.N * sizeof(float));
+  off = align_up(off + (sp.n_splits > 1 ? (size_t)units * sp.n_splits * g.N * sizeof(float) : 0));
+  w.done = off;
+  off = align_up(off + (size_t)units * sizeof(uint32_t));
   w.scores = off;
   off = align_up(off + (size_t)units * g.N * sizeof(float));
   w.discrete = off;
@@ -101,16 +109,17 @@ bool pools_ok(const void* const* pools, int n_layers) {
   return true;
 }
 
-// Scores + partial column sums for every layer (after validation).
+// Window scores of every layer (after validation zeroed `done`).
 hipError_t run_score(const Geom& g, const ScorePlan& sp, int n_layers, const void* q,
                      const void* const* k_pools, const int32_t* trig, const int32_t* bt,
                      const int32_t* win_start, const int32_t* status, float* partials,
-                     hipStream_t stream) {
+                     float* scores, uint32_t* done, hipStream_t stream) {
   const int64_t q_layer = (int64_t)g.n_trig * g.W * g.Hq * g.d * g.esize;
-  const int64_t p_layer = (int64_t)g.n_trig * g.Hkv * sp.n_splits * g.N;
+  const int64_t units_layer = (int64_t)g.n_trig * g.Hkv;
   return for_layer_chunks(n_layers, k_pools, nullptr, [&](int l0, int cnt, const PoolPtrs& kp, const PoolPtrs&) {
     return launch_score(g, sp, cnt, (const char*)q + l0 * q_layer, kp, trig, bt, win_start, status,
-                        partials + l0 * p_layer, stream);
+                        partials + l0 * units_layer * sp.n_splits * g.N, scores + l0 * units_layer * g.N,
+                        done + l0 * units_layer, stream);
   });
 }
 
@@ -162,7 +171,8 @@ kara_status_t kara_validate(const kara_params_t* p, int32_t n_trig, const int32_
   if (st != KARA_OK) return st;
   if (n_trig == 0) return KARA_OK;
   if (!trig || !block_table || !seq_lens || !win_start || !status) return KARA_ERR_INVALID_ARG;
-  return hip_status(launch_validate(g, trig, block_table, seq_lens, win_start, status, (hipStream_t)stream));
+  return hip_status(
+      launch_validate(g, trig, block_table, seq_lens, win_start, status, nullptr, 0, (hipStream_t)stream));
 }
 
 kara_status_t kara_score_window(const kara_params_t* p, int32_t n_trig, const int32_t* trig,
@@ -183,12 +193,12 @@ kara_status_t kara_score_window(const kara_params_t* p, int32_t n_trig, const in
   const WsLayout wl = ws_layout(g, n_layers, sp);
   if (!workspace || workspace_bytes < wl.total) return KARA_ERR_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, s);
-  if (e != hipSuccess) return KARA_ERR_HIP;
-  float* partials = sp.n_splits == 1 ? scores : (float*)((char*)workspace + wl.partials);
-  e = run_score(g, sp, n_layers, q, k_pools, trig, block_table, win_start, status, partials, s);
-  if (e != hipSuccess) return KARA_ERR_HIP;
-  if (sp.n_splits > 1) e = launch_reduce_splits(g, units, sp.n_splits, partials, scores, s);
+  char* ws = (char*)workspace;
+  uint32_t* done = (uint32_t*)(ws + wl.done);
+  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, done, units, s);
+  if (e == hipSuccess)
+    e = run_score(g, sp, n_layers, q, k_pools, trig, block_table, win_start, status, (float*)(ws + wl.partials),
+                  scores, done, s);
   return hip_status(e);
 }
 
@@ -200,8 +210,8 @@ kara_status_t kara_select(const kara_params_t* p, int64_t n_units, const float* 
   if (n_units < 0 || n_units > INT32_MAX) return KARA_ERR_INVALID_ARG;
   if (n_units == 0) return KARA_OK;
   if (!scores || !discrete) return KARA_ERR_INVALID_ARG;
-  return hip_status(launch_select(g, n_units, kSelectDiscrete, nullptr, 1, const_cast<float*>(scores),
-                                  nullptr, discrete, nullptr, (hipStream_t)stream));
+  return hip_status(launch_select(g, n_units, kSelectDiscrete, scores, nullptr, discrete, nullptr,
+                                  (hipStream_t)stream));
 }
 
 kara_status_t kara_token2chunk(const kara_params_t* p, int64_t n_units, const float* scores,
@@ -212,8 +222,8 @@ kara_status_t kara_token2chunk(const kara_params_t* p, int64_t n_units, const fl
   if (n_units < 0 || n_units > INT32_MAX) return KARA_ERR_INVALID_ARG;
   if (n_units == 0) return KARA_OK;
   if (!scores || !discrete || !kept) return KARA_ERR_INVALID_ARG;
-  return hip_status(launch_select(g, n_units, kSelectKept, nullptr, 1, const_cast<float*>(scores),
-                                  discrete, nullptr, kept, (hipStream_t)stream));
+  return hip_status(launch_select(g, n_units, kSelectKept, scores, discrete, nullptr, kept,
+                                  (hipStream_t)stream));
 }
 
 kara_status_t kara_compact_pages(const kara_params_t* p, int32_t n_trig, const int32_t* trig,
@@ -230,7 +240,7 @@ kara_status_t kara_compact_pages(const kara_params_t* p, int32_t n_trig, const i
       !pools_ok((const void* const*)k_pools, n_layers) || !pools_ok((const void* const*)v_pools, n_layers))
     return KARA_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, s);
+  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, nullptr, 0, s);
   if (e == hipSuccess) e = launch_check_kept(g, n_layers, kept, status, s);
   if (e == hipSuccess)
     e = run_compact(g, n_layers, trig, kept, k_pools, v_pools, block_table, seq_lens, win_start, status, s);
@@ -248,7 +258,7 @@ kara_status_t kara_commit_tables(const kara_params_t* p, int32_t n_trig, const i
   if (!trig || !block_table || !seq_lens || !win_start || !freed || !n_freed || !status)
     return KARA_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, s);
+  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, nullptr, 0, s);
   if (e == hipSuccess) e = launch_commit(g, trig, block_table, seq_lens, win_start, freed, n_freed, status, s);
   return hip_status(e);
 }
@@ -276,16 +286,17 @@ kara_status_t kara_compress_window(const kara_params_t* p, int32_t n_trig, const
   if (!workspace || workspace_bytes < wl.total) return KARA_ERR_WORKSPACE;
   char* ws = (char*)workspace;
   float* partials = (float*)(ws + wl.partials);
+  uint32_t* done = (uint32_t*)(ws + wl.done);
+  float* scores_buf = scores ? scores : (float*)(ws + wl.scores);
   int32_t* kept_buf = kept ? kept : (int32_t*)(ws + wl.kept);
   hipStream_t s = (hipStream_t)stream;
 
-  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, s);
+  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, done, units, s);
   if (e == hipSuccess)
     e = run_score(g, sp, n_layers, q, (const void* const*)k_pools, trig, block_table, win_start, status,
-                  partials, s);
+                  partials, scores_buf, done, s);
   if (e == hipSuccess)
-    e = launch_select(g, units, kSelectDiscrete | kSelectKept, partials, sp.n_splits, scores, nullptr,
-                      discrete, kept_buf, s);
+    e = launch_select(g, units, kSelectDiscrete | kSelectKept, scores_buf, nullptr, discrete, kept_buf, s);
   if (e == hipSuccess)
     e = run_compact(g, n_layers, trig, kept_buf, k_pools, v_pools, block_table, seq_lens, win_start,
                     status, s);

@@ -30,12 +30,15 @@ struct PoolPtrs {
   void* p[kMaxLayersPerLaunch];
 };
 
-// Validation kernel (kara_validate.hip).
+// Validation kernel (kara_pages.hip); also zeroes `n_zero` counters at
+// `zero` (may be null) for the scoring kernel's split bookkeeping.
 hipError_t launch_validate(const Geom& g, const int32_t* trig, const int32_t* block_table,
                            const int32_t* seq_lens, const int32_t* win_start, int32_t* status,
-                           hipStream_t stream);
+                           uint32_t* zero, int64_t n_zero, hipStream_t stream);
 
-// Scoring (kara_score.hip): partial column sums, one slab per row split.
+// Scoring (kara_score.hip): per unit, n_splits workgroups each write a
+// partial column sum; the last to finish adds them in split order into
+// `scores` (with one split the workgroup writes `scores` directly).
 struct ScorePlan {
   int cg, rg, nt;       // column groups, row groups, 16-key tiles per wave
   int n_rb;             // 16*rg-row blocks per unit
@@ -46,18 +49,14 @@ ScorePlan plan_score(const Geom& g, int64_t n_units);
 hipError_t launch_score(const Geom& g, const ScorePlan& sp, int n_layers, const void* q,
                         const PoolPtrs& k_pools, const int32_t* trig, const int32_t* block_table,
                         const int32_t* win_start, const int32_t* status, float* partials,
-                        hipStream_t stream);
-hipError_t launch_reduce_splits(const Geom& g, int64_t n_units, int n_splits, const float* partials,
-                                float* scores, hipStream_t stream);
+                        float* scores, uint32_t* done, hipStream_t stream);
 
 // Selection (kara_select.hip).  mode bit 1: discrete top-k; bit 2: Token2Chunk
-// + fill.  Scores come either from `scores` or, when `partials` is non-null,
-// from the partial column sums (n_splits slabs per unit), in which case the
-// reduced scores are also written to `scores` if it is non-null.
+// + fill (from discrete_in when bit 1 is clear).
 enum { kSelectDiscrete = 1, kSelectKept = 2 };
-hipError_t launch_select(const Geom& g, int64_t n_units, int mode, const float* partials,
-                         int n_splits, float* scores, const int32_t* discrete_in,
-                         int32_t* discrete_out, int32_t* kept_out, hipStream_t stream);
+hipError_t launch_select(const Geom& g, int64_t n_units, int mode, const float* scores,
+                         const int32_t* discrete_in, int32_t* discrete_out, int32_t* kept_out,
+                         hipStream_t stream);
 
 // Compaction and metadata (kara_pages.hip).
 hipError_t launch_check_kept(const Geom& g, int n_layers, const int32_t* kept, int32_t* status,

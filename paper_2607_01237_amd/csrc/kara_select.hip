@@ -129,28 +129,16 @@ __device__ void select_top(const KeyT (&key)[kSelEpt], const bool (&elig)[kSelEp
 }
 
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
-    Geom g, int mode, const float* __restrict__ partials, int n_splits, float* __restrict__ scores,
-    const int32_t* __restrict__ disc_in, int32_t* __restrict__ disc_out,
-    int32_t* __restrict__ kept_out) {
+    Geom g, int mode, const float* __restrict__ scores, const int32_t* __restrict__ disc_in,
+    int32_t* __restrict__ disc_out, int32_t* __restrict__ kept_out) {
   __shared__ SelSmem sm;
   const int64_t u = blockIdx.x;
   const int N = g.N;
   const int tid = threadIdx.x;
   const int k = g.k_disc;
 
-  // Scores of the unit: the fixed-order sum of the partial column sums, or
-  // the caller's scores.
   for (int j = tid; j < N; j += kSelThreads) {
-    float v;
-    if (partials) {
-      const float* pp = partials + u * n_splits * (int64_t)N + j;
-      v = pp[0];
-      for (int s = 1; s < n_splits; ++s) v += pp[(int64_t)s * N];
-      if (scores) scores[u * N + j] = v;
-    } else {
-      v = scores[u * N + j];
-    }
-    sm.a[j] = v;
+    sm.a[j] = scores[u * N + j];
     sm.mark[j] = 0;
   }
   __syncthreads();
@@ -271,37 +259,16 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   }
 }
 
-__global__ void reduce_splits_kernel(int64_t n, int N, int n_splits, const float* __restrict__ partials,
-                                     float* __restrict__ scores) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  const int64_t u = i / N;
-  const int j = (int)(i % N);
-  const float* pp = partials + u * n_splits * (int64_t)N + j;
-  float v = pp[0];
-  for (int s = 1; s < n_splits; ++s) v += pp[(int64_t)s * N];
-  scores[i] = v;
-}
-
 }  // namespace
 
-hipError_t launch_select(const Geom& g, int64_t n_units, int mode, const float* partials,
-                         int n_splits, float* scores, const int32_t* discrete_in,
-                         int32_t* discrete_out, int32_t* kept_out, hipStream_t stream) {
+hipError_t launch_select(const Geom& g, int64_t n_units, int mode, const float* scores,
+                         const int32_t* discrete_in, int32_t* discrete_out, int32_t* kept_out,
+                         hipStream_t stream) {
   if (n_units <= 0) return hipSuccess;
-  hipLaunchKernelGGL(select_kernel, dim3((unsigned)n_units), dim3(kSelThreads), 0, stream, g, mode,
-                     partials, n_splits, scores, discrete_in, discrete_out, kept_out);
+  hipLaunchKernelGGL(select_kernel, dim3((unsigned)n_units), dim3(kSelThreads), 0, stream, g, mode, scores,
+                     discrete_in, discrete_out, kept_out);
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_splits(const Geom& g, int64_t n_units, int n_splits, const float* partials,
-                                float* scores, hipStream_t stream) {
-  const int64_t n = n_units * g.N;
-  if (n <= 0) return hipSuccess;
-  const int threads = 256;
-  hipLaunchKernelGGL(reduce_splits_kernel, dim3((unsigned)((n + threads - 1) / threads)), dim3(threads), 0,
-                     stream, n, g.N, n_splits, partials, scores);
-  return hipGetLastError();
-}
 
 }  // namespace kara
