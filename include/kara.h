@@ -128,6 +128,13 @@ const char* kara_status_string(int32_t status);
 int32_t kara_abi_version(void);
 
 /*
+ * Text of the HIP error behind the most recent KARA_ERR_HIP returned on the
+ * calling thread ("no HIP error" if there was none).  Static storage; never
+ * freed by the caller.
+ */
+const char* kara_last_hip_error(void);
+
+/*
  * Bytes of device workspace kara_score_window / kara_compress_window need for
  * this geometry, n_trig triggered sequences and n_layers layers (written to
  * *bytes, a HOST pointer).  Holds partial column sums of Eq. (4) and, for

@@ -82,7 +82,14 @@ WsLayout ws_layout(const Geom& g, int n_layers, const ScorePlan& sp) {
   return w;
 }
 
-kara_status_t hip_status(hipError_t e) { return e == hipSuccess ? KARA_OK : KARA_ERR_HIP; }
+// the last HIP error a call on this thread failed with (hipSuccess: none)
+thread_local hipError_t t_last_hip_error = hipSuccess;
+
+kara_status_t hip_status(hipError_t e) {
+  if (e == hipSuccess) return KARA_OK;
+  t_last_hip_error = e;
+  return KARA_ERR_HIP;
+}
 
 // Runs fn(layer0, count, pool-pointer structs) over chunks of at most
 // kMaxLayersPerLaunch layers.
@@ -151,6 +158,10 @@ const char* kara_status_string(int32_t s) {
 }
 
 int32_t kara_abi_version(void) { return KARA_ABI_VERSION; }
+
+const char* kara_last_hip_error(void) {
+  return t_last_hip_error == hipSuccess ? "no HIP error" : hipGetErrorString(t_last_hip_error);
+}
 
 kara_status_t kara_workspace_size(const kara_params_t* p, int32_t n_trig, int32_t n_layers,
                                   size_t* bytes) {

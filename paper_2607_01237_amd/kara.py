@@ -64,6 +64,7 @@ _PAR = ctypes.POINTER(KaraParams)
 _SIGS = {
     "kara_status_string": (ctypes.c_char_p, [_I32]),
     "kara_abi_version": (_I32, []),
+    "kara_last_hip_error": (ctypes.c_char_p, []),
     "kara_workspace_size": (_I32, [_PAR, _I32, _I32, ctypes.POINTER(ctypes.c_size_t)]),
     "kara_validate": (_I32, [_PAR, _I32, _VP, _VP, _VP, _VP, _VP, _VP]),
     "kara_score_window": (_I32, [_PAR, _I32, _VP, _I32, _VP, _PP, _VP, _VP, _VP, _VP, _VP, _VP,
@@ -91,6 +92,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         return _lib
     if not os.path.exists(path):
         raise KaraError("load", ERR_HIP, f"{path} is not built; run paper_2607_01237_amd.build")
+    # torch ships its own copy of the HIP runtime.  It must be the one loaded
+    # when the library resolves libamdhip64, or the library would start a
+    # second runtime that cannot see torch's memory and streams.
+    import torch  # noqa: F401
     try:
         lib = ctypes.CDLL(path)
     except OSError as e:
@@ -109,7 +114,10 @@ def status_string(code: int) -> str:
 
 def _check(fn: str, code: int):
     if code != OK:
-        raise KaraError(fn, code, status_string(code))
+        msg = status_string(code)
+        if code == ERR_HIP:
+            msg += f" [{load().kara_last_hip_error().decode()}]"
+        raise KaraError(fn, code, msg)
 
 
 def _ptr(t):

@@ -29,7 +29,7 @@ def good_params(**kw):
 
 def test_exports_every_declared_function(lib):
     names = kara.header_functions()
-    assert len(names) == 10
+    assert len(names) == 11
     for n in names:
         assert hasattr(lib, n), n
 
@@ -39,6 +39,8 @@ def test_version_and_status_strings(lib):
     for code in (0, -1, -2, -3, -4):
         assert kara.status_string(code).startswith("KARA_")
     assert "unknown" in kara.status_string(12345)
+    # nothing has failed on this thread: no HIP call is made to say so
+    assert lib.kara_last_hip_error() == b"no HIP error"
 
 
 def test_workspace_size_scales(lib):
