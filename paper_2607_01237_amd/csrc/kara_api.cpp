@@ -61,7 +61,7 @@ kara_status_t make_geom(const kara_params_t* p, int32_t n_trig, Geom* g) {
 inline size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct WsLayout {
-  size_t partials, done, scores, discrete, kept, total;
+  size_t partials, scores, discrete, kept, total;
 };
 
 WsLayout ws_layout(const Geom& g, int n_layers, const ScorePlan& sp) {
@@ -70,8 +70,6 @@ WsLayout ws_layout(const Geom& g, int n_layers, const ScorePlan& sp) {
   size_t off = 0;
   w.partials = off;
   off = align_up(off + (sp.n_splits > 1 ? (size_t)units * sp.n_splits * g.N * sizeof(float) : 0));
-  w.done = off;
-  off = align_up(off + (size_t)units * sizeof(uint32_t));
   w.scores = off;
   off = align_up(off + (size_t)units * g.N * sizeof(float));
   w.discrete = off;
@@ -116,17 +114,17 @@ bool pools_ok(const void* const* pools, int n_layers) {
   return true;
 }
 
-// Window scores of every layer (after validation zeroed `done`).
+// Window scores of every layer.
 hipError_t run_score(const Geom& g, const ScorePlan& sp, int n_layers, const void* q,
                      const void* const* k_pools, const int32_t* trig, const int32_t* bt,
                      const int32_t* win_start, const int32_t* status, float* partials,
-                     float* scores, uint32_t* done, hipStream_t stream) {
+                     float* scores, hipStream_t stream) {
   const int64_t q_layer = (int64_t)g.n_trig * g.W * g.Hq * g.d * g.esize;
   const int64_t units_layer = (int64_t)g.n_trig * g.Hkv;
   return for_layer_chunks(n_layers, k_pools, nullptr, [&](int l0, int cnt, const PoolPtrs& kp, const PoolPtrs&) {
     return launch_score(g, sp, cnt, (const char*)q + l0 * q_layer, kp, trig, bt, win_start, status,
                         partials + l0 * units_layer * sp.n_splits * g.N, scores + l0 * units_layer * g.N,
-                        done + l0 * units_layer, stream);
+                        stream);
   });
 }
 
@@ -183,7 +181,7 @@ kara_status_t kara_validate(const kara_params_t* p, int32_t n_trig, const int32_
   if (n_trig == 0) return KARA_OK;
   if (!trig || !block_table || !seq_lens || !win_start || !status) return KARA_ERR_INVALID_ARG;
   return hip_status(
-      launch_validate(g, trig, block_table, seq_lens, win_start, status, nullptr, 0, (hipStream_t)stream));
+      launch_validate(g, trig, block_table, seq_lens, win_start, status, (hipStream_t)stream));
 }
 
 kara_status_t kara_score_window(const kara_params_t* p, int32_t n_trig, const int32_t* trig,
@@ -205,11 +203,10 @@ kara_status_t kara_score_window(const kara_params_t* p, int32_t n_trig, const in
   if (!workspace || workspace_bytes < wl.total) return KARA_ERR_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
   char* ws = (char*)workspace;
-  uint32_t* done = (uint32_t*)(ws + wl.done);
-  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, done, units, s);
+  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, s);
   if (e == hipSuccess)
     e = run_score(g, sp, n_layers, q, k_pools, trig, block_table, win_start, status, (float*)(ws + wl.partials),
-                  scores, done, s);
+                  scores, s);
   return hip_status(e);
 }
 
@@ -251,7 +248,7 @@ kara_status_t kara_compact_pages(const kara_params_t* p, int32_t n_trig, const i
       !pools_ok((const void* const*)k_pools, n_layers) || !pools_ok((const void* const*)v_pools, n_layers))
     return KARA_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, nullptr, 0, s);
+  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, s);
   if (e == hipSuccess) e = launch_check_kept(g, n_layers, kept, status, s);
   if (e == hipSuccess)
     e = run_compact(g, n_layers, trig, kept, k_pools, v_pools, block_table, seq_lens, win_start, status, s);
@@ -269,7 +266,7 @@ kara_status_t kara_commit_tables(const kara_params_t* p, int32_t n_trig, const i
   if (!trig || !block_table || !seq_lens || !win_start || !freed || !n_freed || !status)
     return KARA_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, nullptr, 0, s);
+  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, s);
   if (e == hipSuccess) e = launch_commit(g, trig, block_table, seq_lens, win_start, freed, n_freed, status, s);
   return hip_status(e);
 }
@@ -297,15 +294,14 @@ kara_status_t kara_compress_window(const kara_params_t* p, int32_t n_trig, const
   if (!workspace || workspace_bytes < wl.total) return KARA_ERR_WORKSPACE;
   char* ws = (char*)workspace;
   float* partials = (float*)(ws + wl.partials);
-  uint32_t* done = (uint32_t*)(ws + wl.done);
   float* scores_buf = scores ? scores : (float*)(ws + wl.scores);
   int32_t* kept_buf = kept ? kept : (int32_t*)(ws + wl.kept);
   hipStream_t s = (hipStream_t)stream;
 
-  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, done, units, s);
+  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, s);
   if (e == hipSuccess)
     e = run_score(g, sp, n_layers, q, (const void* const*)k_pools, trig, block_table, win_start, status,
-                  partials, scores_buf, done, s);
+                  partials, scores_buf, s);
   if (e == hipSuccess)
     e = launch_select(g, units, kSelectDiscrete | kSelectKept, scores_buf, nullptr, discrete, kept_buf, s);
   if (e == hipSuccess)

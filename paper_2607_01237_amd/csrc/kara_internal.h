@@ -30,26 +30,23 @@ struct PoolPtrs {
   void* p[kMaxLayersPerLaunch];
 };
 
-// Validation kernel (kara_pages.hip); also zeroes `n_zero` counters at
-// `zero` (may be null) for the scoring kernel's split bookkeeping.
+// Validation kernel (kara_pages.hip).
 hipError_t launch_validate(const Geom& g, const int32_t* trig, const int32_t* block_table,
                            const int32_t* seq_lens, const int32_t* win_start, int32_t* status,
-                           uint32_t* zero, int64_t n_zero, hipStream_t stream);
+                           hipStream_t stream);
 
 // Scoring (kara_score.hip): per unit, n_splits workgroups each write a
 // partial column sum; the last to finish adds them in split order into
 // `scores` (with one split the workgroup writes `scores` directly).
 struct ScorePlan {
-  int cg, rg, nt;       // column groups, row groups, 16-key tiles per wave
-  int n_rb;             // 16*rg-row blocks per unit
-  int n_splits;         // row splits per unit
-  int n_cols;           // padded column count cg * nt * 16
+  int rows_wg;          // query rows per workgroup
+  int n_splits;         // row splits (workgroups) per unit
 };
 ScorePlan plan_score(const Geom& g, int64_t n_units);
 hipError_t launch_score(const Geom& g, const ScorePlan& sp, int n_layers, const void* q,
                         const PoolPtrs& k_pools, const int32_t* trig, const int32_t* block_table,
                         const int32_t* win_start, const int32_t* status, float* partials,
-                        float* scores, uint32_t* done, hipStream_t stream);
+                        float* scores, hipStream_t stream);
 
 // Selection (kara_select.hip).  mode bit 1: discrete top-k; bit 2: Token2Chunk
 // + fill (from discrete_in when bit 1 is clear).

@@ -8,10 +8,8 @@ namespace {
 
 __global__ void validate_kernel(Geom g, const int32_t* __restrict__ trig,
                                 const int32_t* __restrict__ bt, const int32_t* __restrict__ seq_lens,
-                                const int32_t* __restrict__ win_start, int32_t* __restrict__ status,
-                                uint32_t* __restrict__ zero, int64_t n_zero) {
+                                const int32_t* __restrict__ win_start, int32_t* __restrict__ status) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n_zero) zero[i] = 0;
   if (i >= g.n_trig) return;
   const int t = (int)i;
   const int s = trig[t];
@@ -153,12 +151,11 @@ __global__ void commit_kernel(Geom g, const int32_t* __restrict__ trig, int32_t*
 
 hipError_t launch_validate(const Geom& g, const int32_t* trig, const int32_t* block_table,
                            const int32_t* seq_lens, const int32_t* win_start, int32_t* status,
-                           uint32_t* zero, int64_t n_zero, hipStream_t stream) {
+                           hipStream_t stream) {
   const int threads = 256;
-  const int64_t n = n_zero > g.n_trig ? n_zero : g.n_trig;
-  const int64_t blocks = (n + threads - 1) / threads;
+  const int64_t blocks = ((int64_t)g.n_trig + threads - 1) / threads;
   hipLaunchKernelGGL(validate_kernel, dim3((unsigned)blocks), dim3(threads), 0, stream, g, trig, block_table,
-                     seq_lens, win_start, status, zero, n_zero);
+                     seq_lens, win_start, status);
   return hipGetLastError();
 }
 

@@ -2,22 +2,30 @@
 // per (sequence, layer, KV head), all G query heads of the group acting as
 // queries of their KV head.
 //
-// Single pass over the logits.  A workgroup of 8 waves owns 32*RG query rows
-// at a time and all N = W-U keys, split over CG column groups (CG*RG = 8).
-// Every wave holds the logits of its 32 rows x 16*NT keys in registers; its
-// two 16-row MFMA tiles share each key operand read from LDS.  Keys (and the
-// next row block's queries) stream into LDS by direct global->LDS copies
-// through a three-stage ring, so no register is spent on staging and the
-// copies of later chunks overlap the MFMAs and exponentials of the current
-// one.  Per chunk each lane updates a running row maximum over its own keys
-// (earlier exponentials are rescaled only when a chunk exceeds it by more
-// than 2^32), exponentiates and accumulates row sums; once all keys are
-// seen, row maximum and sum are combined across lanes (shuffles) and column
-// groups (LDS), and each lane adds its rows' normalised probabilities to
-// fixed per-(lane group, column) slots in LDS.  The workgroup finally
-// reduces those slots in a fixed order and writes one partial column sum per
-// row split; the selection kernel adds the splits in order.  No
+// Two sweeps over the keys per workgroup.  A workgroup of 8 waves owns 128*RT
+// query rows of one unit (16*RT rows per wave, held as MFMA operands in
+// registers for the whole kernel) and streams the unit's N keys through an
+// LDS ring, 64 keys per chunk, twice:
+//   sweep A  logits -> per-row maximum and exponential sum (log-sum-exp),
+//   sweep B  logits again -> normalised probabilities -> column sums.
+// Every wave sees every key of its own rows, so the row statistics need no
+// exchange between waves.  Recomputing the logits doubles the matrix work
+// but keeps nothing per logit between the sweeps, so the rows sharing one
+// read of the keys (512 for bf16) are limited by the operand registers only;
+// a single sweep would have to hold every logit of its rows in registers and
+// re-read all keys for every 32 rows.  Keys reach LDS by direct global->LDS
+// copies, so no register is spent on staging and the copies of later chunks
+// overlap the matrix and exponential work of the current one.
+//
+// Column sums of a chunk are reduced within each wave in a fixed lane order,
+// then across the 8 waves in wave order into a per-workgroup row in LDS.
+// Each workgroup writes one partial sum per row split and a second kernel
+// adds them in split order.  (Handing the sum to the last split to finish
+// would need a device-scope release/acquire, which on this multi-XCD part
+// writes back and invalidates the whole L2 of the XCD every time.)  No
 // floating-point atomics, so the scores are bit-reproducible.
+#include <type_traits>
+
 #include "kara_internal.h"
 
 namespace kara {
@@ -29,8 +37,18 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 constexpr int kScoreThreads = 512;
 constexpr int kScoreWaves = kScoreThreads / 64;
 constexpr int kLdsLimit = 160 * 1024;
+constexpr int kTps = 4;                   // 16-key tiles per chunk
+constexpr int kChunkKeys = kTps * 16;     // keys per chunk
+constexpr int kMaxChunks = (KARA_MAX_COMPRESSIBLE + kChunkKeys - 1) / kChunkKeys;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_huge_valf();
+constexpr float kPosInf = __builtin_huge_valf();
+// Lower end of a running row maximum (log2 units): finite, so that
+// exp2(m_old - m_new) never sees inf - inf.
+constexpr float kMaxFloor = -1e30f;
+// Sweep A accumulates exp2(x - m) against a maximum m that is only raised
+// when a row sum would pass this bound, so no term or sum can overflow.
+constexpr float kSumBound = 18446744073709551616.f;   // 2^64
 
 struct ScoreArgs {
   Geom g;
@@ -42,55 +60,30 @@ struct ScoreArgs {
   const int32_t* status;
   float* partials;            // [units][n_splits][N] (unused with one split)
   float* scores;              // [units][N]
-  uint32_t* done;             // [units] splits finished; zeroed by the validation kernel
-  int n_splits, n_rb;
+  int n_splits;
   int64_t n_blocks;
 };
 
-// Static geometry of one kernel instance.
-template <int DT, int D, int NT, int CG>
+// Static geometry of one kernel instance: element type DT, head dim D, RT
+// 16-row tiles per wave.
+template <int DT, int D, int RT>
 struct Cfg {
   static constexpr int kES = DT == KARA_BF16 ? 2 : 4;
-  static constexpr int kRowBytes = D * kES;             // one key or query row
+  static constexpr int kRowBytes = D * kES;              // one key or query row
   static constexpr int kCPR = kRowBytes / 16;            // 16-byte chunks per row
   static constexpr int kSwz = kCPR < 16 ? kCPR - 1 : 15; // XOR swizzle mask
-  static constexpr int kRG = kScoreWaves / CG;
-  static constexpr int kRows = 32 * kRG;                 // query rows per row block
-  static constexpr int kNCol = CG * NT * 16;
-  static constexpr int kPartBytes = kRG * kNCol * 4;
-  static constexpr int kSmallBytes = kNCol * 4 + 2 * kRG * CG * 32 * 4;
-  // query tile, padded so every thread issues the same number of copies
-  static constexpr int kQL = (kRows * kCPR + kScoreThreads - 1) / kScoreThreads;
-  static constexpr int kQBytes = kQL * kScoreThreads * 16;
-  // key chunks: TPS 16-key tiles per column group, kStages stages in a ring;
-  // the stage of a chunk must be a compile-time function of the chunk index,
-  // so kStages divides the chunks per row block
-  static constexpr int kTpsMin0 = kScoreThreads / (16 * kCPR * CG);
-  static constexpr int kTpsMin = kTpsMin0 < 1 ? 1 : kTpsMin0;
-  static constexpr int stages_for(int tps) {
-    return (NT / tps) % 4 == 0 ? 4 : (NT / tps) % 2 == 0 ? 2 : 1;
+  static constexpr int kRowsWG = kScoreWaves * 16 * RT;  // query rows per workgroup
+  static constexpr int kStageBytes = kChunkKeys * kRowBytes;
+  static constexpr int kL = kStageBytes / (kScoreThreads * 16);   // copies per thread per chunk
+  static constexpr int kFixedBytes = 2 * kMaxChunks * kChunkKeys * 4 + 2 * kScoreWaves * kChunkKeys * 4;
+  static constexpr int fit_stages() {
+    int s = 6;
+    while (s > 2 && s * kStageBytes + kFixedBytes > kLdsLimit) --s;
+    return s;
   }
-  static constexpr int lds_bytes(int tps) {
-    return stages_for(tps) * CG * tps * 16 * kRowBytes + kQBytes + kPartBytes + kSmallBytes;
-  }
-  static constexpr int fit_tps() {
-    int tps = (32768 / kRowBytes / 16) / CG;           // ~32 KB stages
-    if (tps > NT / 4) tps = NT / 4;                    // at least four chunks per row block
-    if (tps < kTpsMin) tps = kTpsMin;
-    if (tps > NT) tps = NT;
-    while (tps > kTpsMin && lds_bytes(tps) > kLdsLimit) tps /= 2;
-    return tps;
-  }
-  static constexpr int kTPS = fit_tps();
-  static constexpr int kStages = stages_for(kTPS);
-  static constexpr int kKeys = CG * kTPS * 16;           // keys per stage
-  static constexpr int kStageBytes = kKeys * kRowBytes;
-  static constexpr int kL = kKeys * kCPR / kScoreThreads; // copies per thread per stage
-  static constexpr int kNCH = NT / kTPS;                  // chunks per row block
-  static_assert(NT % kTPS == 0, "chunks must tile the wave's keys");
-  static_assert(kNCH % kStages == 0, "stage index must be static");
-  static_assert((kKeys * kCPR) % kScoreThreads == 0, "stage copies must be uniform over threads");
-  static_assert(lds_bytes(kTPS) <= kLdsLimit, "LDS budget");
+  static constexpr int kStages = fit_stages();
+  static_assert(kL >= 1 && kL * kScoreThreads * 16 == kStageBytes, "chunk copies must be uniform over threads");
+  static_assert(kStages * kStageBytes + kFixedBytes <= kLdsLimit, "LDS budget");
 };
 
 // A lane's operand: lane group gq = lane/16 supplies head-dim elements
@@ -124,6 +117,7 @@ __device__ inline floatx4 dot_tile(const Operand<DT, D>& qa, const Operand<DT, D
   return acc;
 }
 
+// reductions over the 16 lanes of a lane group (the 16 keys of a tile)
 __device__ inline float max16(float v) {
 #pragma unroll
   for (int o = 1; o < 16; o <<= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
@@ -139,7 +133,8 @@ __device__ inline float sum16(float v) {
 // lds_wave_base + 16*i (global_load_lds_dwordx4 with the LDS base in M0).
 // Issued through inline assembly: the compiler then inserts no wait of its
 // own before LDS reads (it cannot tell the ring stages apart and would drain
-// every copy); the kernel waits explicitly with wait_vm().  M0 is restored.
+// every copy); the kernel waits explicitly with wait_chunks().  M0 is
+// restored.
 __device__ inline void copy16(const void* g, char* lds_wave_base) {
   const uint32_t lds = __builtin_amdgcn_readfirstlane(
       (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_wave_base);
@@ -157,7 +152,7 @@ __device__ inline void copy16(const void* g, char* lds_wave_base) {
 // Workgroup barrier for LDS traffic only.  __syncthreads() would also drain
 // every outstanding global->LDS copy (its release fence waits on vmcnt),
 // defeating the prefetch ring; the copies this barrier must cover are waited
-// for explicitly with wait_vm() first.
+// for explicitly first.
 __device__ inline void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
@@ -167,37 +162,41 @@ __device__ inline void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-template <int DT, int D, int NT, int CG>
+// Wait until at most kL*newer of this thread's memory operations are
+// outstanding, newer <= P-1 (a run-time count, compile-time wait fields).
+template <int kL, int P>
+__device__ inline void wait_chunks(int newer) {
+  if constexpr (P >= 6) { if (newer >= 5) { wait_vm<5 * kL>(); return; } }
+  if constexpr (P >= 5) { if (newer >= 4) { wait_vm<4 * kL>(); return; } }
+  if constexpr (P >= 4) { if (newer >= 3) { wait_vm<3 * kL>(); return; } }
+  if constexpr (P >= 3) { if (newer >= 2) { wait_vm<2 * kL>(); return; } }
+  if constexpr (P >= 2) { if (newer >= 1) { wait_vm<kL>(); return; } }
+  wait_vm<0>();
+}
+
+template <int DT, int D, int RT>
 __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
-  using C = Cfg<DT, D, NT, CG>;
+  using C = Cfg<DT, D, RT>;
   using Op = Operand<DT, D>;
-  constexpr int RG = C::kRG;
-  constexpr int TPS = C::kTPS;
-  constexpr int NCH = C::kNCH;
   constexpr int CPR = C::kCPR;
   constexpr int S = C::kStages;
   constexpr int P = S - 1;                // prefetch distance in chunks
-  constexpr int kL = C::kL, kQL = C::kQL;
+  constexpr int kL = C::kL;
   constexpr int KC = Op::kChunks;
-  constexpr bool kEarlyQ = S == 4;        // next row block's queries fetched at chunk 1
+  static_assert(P <= 6, "wait_chunks covers at most six chunks in flight");
 
   __shared__ __attribute__((aligned(16))) char kbuf[S * C::kStageBytes];
-  __shared__ __attribute__((aligned(16))) char qbuf[C::kQBytes];
-  // column sums of this workgroup's rows, per row group; slot (rg, column)
-  // is updated by exactly one lane after each row block
-  __shared__ float part[RG][C::kNCol];
-  __shared__ float red_max[RG][CG][32];
-  __shared__ float red_sum[RG][CG][32];
   // byte offset / 16 of every compressible key row in the K pool (the block
-  // table resolved once per workgroup); padding entries repeat row 0
-  __shared__ uint32_t key_off[C::kNCol];
+  // table resolved once per workgroup); padding entries repeat key 0
+  __shared__ uint32_t key_off[kMaxChunks * kChunkKeys];
+  // this workgroup's column sums; per-wave column sums of the last three chunks
+  __shared__ float col_wg[kMaxChunks * kChunkKeys];
+  __shared__ float col_wave[3][kScoreWaves][kChunkKeys];
 
   const Geom& g = a.g;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform, kept in an SGPR
-  const int cg = wave % CG;
-  const int rg = wave / CG;
   const int gq = lane >> 4;     // lane group: rows 4*gq..4*gq+3 of a 16-row tile
   const int li = lane & 15;     // key of a 16-key tile / row of the query operand
 
@@ -212,304 +211,341 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
   const int t = (int)((u / g.Hkv) % g.n_trig);
   const int l = (int)(u / ((int64_t)g.Hkv * g.n_trig));
   const int N = g.N;
+  const int nch = (N + kChunkKeys - 1) / kChunkKeys;
   float* out = a.n_splits == 1 ? a.scores + u * (int64_t)N : a.partials + (u * a.n_splits + split) * (int64_t)N;
 
   if (a.status[t] != 0) {
-    float* sc = a.scores + u * (int64_t)N;
-    for (int j = tid; j < N; j += kScoreThreads) sc[j] = 0.f;
+    for (int j = tid; j < N; j += kScoreThreads) out[j] = 0.f;
     return;
   }
   const int s = a.trig[t];
   const int p0 = a.win_start[s];
-  {
-    const int32_t* row_pages = a.bt + (int64_t)s * g.max_blocks;
-    for (int j = tid; j < C::kNCol; j += kScoreThreads) {
-      const int pos = p0 + (j < N ? j : 0);        // padding keys: any valid row
-      const uint64_t row = ((uint64_t)row_pages[pos / g.bs] * g.Hkv + h) * g.bs + pos % g.bs;
-      key_off[j] = (uint32_t)(row * (C::kRowBytes / 16));
-    }
-    for (int i = tid; i < RG * C::kNCol; i += kScoreThreads) (&part[0][0])[i] = 0.f;
-  }
-  // the key offsets must be in LDS before the copies below compute addresses
-  lds_barrier();
-
   const char* kpool = (const char*)a.k.p[l];
   const char* qunit = a.q + ((int64_t)l * g.n_trig + t) * g.W * g.Hq * (int64_t)C::kRowBytes;
   const int R = g.G * g.W;
   const float c = g.scale * kLog2e;
 
-  // ---- copies into LDS (every thread issues exactly kL / kQL per call) ----
-  // Key copy r of this thread fills stage slot r*512 + tid: key row
-  // kr = slot / CPR of the stage, 16-byte chunk (slot % CPR) ^ (kr & kSwz).
-  // Only the key index depends on the chunk, by a compile-time step, so per
-  // copy the address costs one LDS read of the key table and one shift-add.
+  // ---- this wave's query rows, straight into operand registers ----
+  // row r = w*G + gi (window token w, query head h*G + gi); rows past R
+  // repeat row 0 and are given no weight
+  const int row_base = split * C::kRowsWG + wave * 16 * RT;
+  Op qa[RT];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    int r = row_base + rt * 16 + li;
+    if (r >= R) r = 0;
+    const int w = r / g.G, gi = r - w * g.G;
+    const uint4* src = (const uint4*)(qunit + ((int64_t)w * g.Hq + h * g.G + gi) * C::kRowBytes) + gq * KC;
+#pragma unroll
+    for (int ks = 0; ks < KC; ++ks) qa[rt].v[ks] = src[ks];
+  }
+  // Consume the query registers here, before any key copy is issued, so the
+  // compiler waits for these loads once.  Otherwise it keeps them pending
+  // into the chunk loops and waits on them there with counts that cannot
+  // see the copies in flight, draining the key ring every chunk.
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int ks = 0; ks < KC; ++ks) asm volatile("" ::"v"(qa[rt].v[ks].x), "v"(qa[rt].v[ks].y),
+                                                 "v"(qa[rt].v[ks].z), "v"(qa[rt].v[ks].w));
+
+  {
+    const int32_t* row_pages = a.bt + (int64_t)s * g.max_blocks;
+    for (int j = tid; j < nch * kChunkKeys; j += kScoreThreads) {
+      const int pos = p0 + (j < N ? j : 0);        // padding keys: any valid row
+      const uint64_t row = ((uint64_t)row_pages[pos / g.bs] * g.Hkv + h) * g.bs + pos % g.bs;
+      key_off[j] = (uint32_t)(row * (C::kRowBytes / 16));
+    }
+  }
+  // the key offsets must be in LDS before the copies below compute addresses
+  lds_barrier();
+
+  // ---- key copies: every thread issues exactly kL per chunk ----
+  // Copy r of this thread fills stage slot r*512 + tid: key row kr = slot /
+  // CPR of the chunk, 16-byte chunk (slot % CPR) ^ (kr & kSwz).  The key
+  // offsets of a chunk are read from the table one iteration before its
+  // copies are issued, so issuing them never waits on LDS.
   const char* kpool_c[kL];
-  int kidx0[kL];
+  int kr0[kL];
 #pragma unroll
   for (int r = 0; r < kL; ++r) {
     const int slot = r * kScoreThreads + tid;
     const int kr = slot / CPR;
     const int chunk = (slot % CPR) ^ (kr & C::kSwz);
     kpool_c[r] = kpool + chunk * 16;
-    kidx0[r] = (kr / (TPS * 16)) * NT * 16 + kr % (TPS * 16);
+    kr0[r] = kr;
   }
-  auto load_keys = [&](int ch, int stage) {
-    char* sbase = kbuf + stage * C::kStageBytes;
+  const int n_it = 2 * nch;                // sweep A, then sweep B, over the same chunks
+  uint32_t coff[kL];
+  auto read_offsets = [&](int it) __attribute__((always_inline)) {
+    const int ch = it < nch ? it : it - nch;
 #pragma unroll
-    for (int r = 0; r < kL; ++r) {
-      const uint32_t off = key_off[kidx0[r] + ch * TPS * 16];
-      copy16(kpool_c[r] + (uint64_t)off * 16, sbase + (r * kScoreWaves + wave) * 1024);
-    }
+    for (int r = 0; r < kL; ++r) coff[r] = key_off[ch * kChunkKeys + kr0[r]];
   };
-  auto load_queries = [&](int rb) {
+  auto issue_copies = [&](int it) __attribute__((always_inline)) {
+    char* sbase = kbuf + (it % S) * C::kStageBytes;
 #pragma unroll
-    for (int r = 0; r < kQL; ++r) {
-      const int slot = r * kScoreThreads + tid;
-      const int row = slot / CPR;
-      const int chunk = (slot % CPR) ^ (row & C::kSwz);
-      int rr = rb * C::kRows + row;
-      if (row >= C::kRows || rr >= R) rr = 0;      // padding rows: any valid row
-      const int w = rr / g.G, gi = rr - w * g.G;
-      const char* src = qunit + ((int64_t)w * g.Hq + h * g.G + gi) * C::kRowBytes + chunk * 16;
-      copy16(src, qbuf + (r * kScoreWaves + wave) * 1024);
-    }
+    for (int r = 0; r < kL; ++r) copy16(kpool_c[r] + (uint64_t)coff[r] * 16, sbase + (r * kScoreWaves + wave) * 1024);
   };
 
-  // per-lane LDS byte offsets of the operand chunks (rows are multiples of 16
-  // plus li, so the swizzle term depends on the lane only)
-  int koff[KC], qoff[KC];
+  // per-lane LDS byte offsets of the key operand chunks (key rows are
+  // multiples of 16 plus li, so the swizzle term depends on the lane only)
+  int koff[KC];
 #pragma unroll
-  for (int ks = 0; ks < KC; ++ks) {
-    const int sw = ((gq * KC + ks) ^ (li & C::kSwz)) * 16;
-    koff[ks] = (cg * TPS * 16 + li) * C::kRowBytes + sw;
-    qoff[ks] = (rg * 32 + li) * C::kRowBytes + sw;
-  }
+  for (int ks = 0; ks < KC; ++ks) koff[ks] = li * C::kRowBytes + (((gq * KC + ks) ^ (li & C::kSwz)) * 16);
 
-  const int rb0 = (int)((int64_t)split * a.n_rb / a.n_splits);
-  const int rb1 = (int)((int64_t)(split + 1) * a.n_rb / a.n_splits);
-  const int n_it = (rb1 - rb0) * NCH;
-
-  // prologue: queries of the first row block, then the first key chunks
-  load_queries(rb0);
+  // logits of this wave's rows x the chunk's 64 keys:
+  // acc[rt][ti][q] = row rt*16 + 4*gq + q, key ti*16 + li
+  floatx4 acc[RT][kTps];
+  auto b_read = [&](const char* sb, int ti, Op& kb) __attribute__((always_inline)) {
 #pragma unroll
-  for (int j = 0; j < (P > 0 ? P : 1); ++j)
-    if (j < n_it) load_keys(j % NCH, j % S);
-
-  Op qa[2];
-  floatx4 acc[2][NT];
-  int it = 0;
-  for (int rb = rb0; rb < rb1; ++rb) {
-    // ---- MFMA phase: all keys of the row block, chunk by chunk ----
+    for (int ks = 0; ks < KC; ++ks) kb.v[ks] = *(const uint4*)(sb + koff[ks] + ti * 16 * C::kRowBytes);
+  };
+  auto mfma_tile = [&](const Op& kb, int ti) __attribute__((always_inline)) {
 #pragma unroll
-    for (int ch = 0; ch < NCH; ++ch, ++it) {
-      // Wait for chunk `it` (and, at a row block start, the queries, issued
-      // before it).  Per thread copies are issued in the order Q(rb0),
-      // K(0..P-1), then per iteration j: [Q(rb+1) if chunk 1] K(j+P); so the
-      // copies still allowed in flight are those of iterations it-P+1..it-1.
-      if constexpr (S == 4) {
-        const int newer_k = (it + 1 < n_it) + (it + 2 < n_it);
-        const bool newer_q = (ch == 2 || ch == 3) && rb + 1 < rb1;
-        if (newer_q) {
-          if (newer_k == 2) wait_vm<2 * kL + kQL>();
-          else if (newer_k == 1) wait_vm<kL + kQL>();
-          else wait_vm<kQL>();
-        } else {
-          if (newer_k == 2) wait_vm<2 * kL>();
-          else if (newer_k == 1) wait_vm<kL>();
-          else wait_vm<0>();
+    for (int rt = 0; rt < RT; ++rt) acc[rt][ti] = dot_tile<DT, D>(qa[rt], kb, floatx4{0.f, 0.f, 0.f, 0.f});
+  };
+
+  // Logits of chunk `it` (its keys are in stage it % S): acc holds this
+  // wave's rows x the chunk's 64 keys; keys past N become -inf.
+  auto form = [&](int it) __attribute__((always_inline)) {
+    const char* sb = kbuf + (it % S) * C::kStageBytes;
+    const int ch = it < nch ? it : it - nch;
+    // one key operand at a time keeps the kernel within 256 registers; the
+    // other wave of the SIMD covers the LDS latency
+#pragma unroll
+    for (int ti = 0; ti < kTps; ++ti) {
+      Op kb;
+      b_read(sb, ti, kb);
+      mfma_tile(kb, ti);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if ((ch + 1) * kChunkKeys > N) {
+#pragma unroll
+      for (int ti = 0; ti < kTps; ++ti)
+        if (ch * kChunkKeys + ti * 16 + li >= N) {
+#pragma unroll
+          for (int rt = 0; rt < RT; ++rt) acc[rt][ti] = floatx4{kNegInf, kNegInf, kNegInf, kNegInf};
         }
-      } else {
-        wait_vm<0>();
+    }
+  };
+
+  // ---- sweep A: per-row reference m and sum l of exp2(x - m), x = logit*c,
+  // over this lane's keys.  The first chunk sets m to the lane's maximum so
+  // far (an exact running-maximum update); later chunks only add terms, which
+  // may then exceed 1.  fp32 holds such sums exactly enough unless a logit
+  // lies about 128 log2-units above m, which makes the sum infinite: a wave
+  // that sees that redoes the sweep on its own with the running maximum.
+  float m[RT][4], lsum[RT][4];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      m[rt][q] = kMaxFloor;
+      lsum[rt][q] = 0.f;
+    }
+  // running-maximum update by one 16-key tile (keys past N are -inf)
+  auto valu_exact = [&](int ti) __attribute__((always_inline)) {
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float x = acc[rt][ti][q] * c;
+        const float mn = fmaxf(m[rt][q], x);
+        lsum[rt][q] = fmaf(lsum[rt][q], __builtin_amdgcn_exp2f(m[rt][q] - mn), __builtin_amdgcn_exp2f(x - mn));
+        m[rt][q] = mn;
       }
-      lds_barrier();
-      if (ch == 0) {
+  };
+  auto valu_a = [&](int ti) __attribute__((always_inline)) {
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-          for (int ks = 0; ks < KC; ++ks) qa[rt].v[ks] = *(const uint4*)(qbuf + qoff[ks] + rt * 16 * C::kRowBytes);
-        if constexpr (!kEarlyQ) {
-          // every wave holds its queries before the buffer is refilled
-          lds_barrier();
-          if (rb + 1 < rb1) load_queries(rb + 1);
+      for (int q = 0; q < 4; ++q) lsum[rt][q] += __builtin_amdgcn_exp2f(fmaf(acc[rt][ti][q], c, -m[rt][q]));
+  };
+  // after sweep A, m[][] holds each row's log-sum-exp (log2 units)
+  auto finish_sweep_a = [&]() __attribute__((always_inline)) {
+    bool bad = false;
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) bad |= !(lsum[rt][q] <= 3.4e38f);
+    if (__builtin_amdgcn_ballot_w64(bad) != 0) {
+      // redo this wave's rows, reading the key operands from global memory
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          m[rt][q] = kMaxFloor;
+          lsum[rt][q] = 0.f;
         }
-      }
-      if constexpr (kEarlyQ) {
-        if (ch == 1 && rb + 1 < rb1) load_queries(rb + 1);
-      }
-      if constexpr (P > 0) {
-        if (it + P < n_it) load_keys((ch + P) % NCH, (ch + P) % S);
-      }
-      // the two 16-row tiles share each key operand
-      const char* sbase = kbuf + (ch % S) * C::kStageBytes;
-#pragma unroll
-      for (int ti = 0; ti < TPS; ++ti) {
+      for (int j0 = 0; j0 < N; j0 += 16) {
+        const int j = j0 + li;
+        const uint4* src = (const uint4*)(kpool + (uint64_t)key_off[j < N ? j : 0] * 16) + gq * KC;
         Op kb;
 #pragma unroll
-        for (int ks = 0; ks < KC; ++ks) kb.v[ks] = *(const uint4*)(sbase + koff[ks] + ti * 16 * C::kRowBytes);
+        for (int ks = 0; ks < KC; ++ks) kb.v[ks] = src[ks];
+        mfma_tile(kb, 0);
+        if (j >= N) {
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
-          acc[rt][ch * TPS + ti] = dot_tile<DT, D>(qa[rt], kb, floatx4{0.f, 0.f, 0.f, 0.f});
-      }
-      if constexpr (P == 0) {
-        // single stage: every wave is done with it before the next copy
-        if (it + 1 < n_it) {
-          lds_barrier();
-          load_keys((ch + 1) % NCH, 0);
+          for (int rt = 0; rt < RT; ++rt) acc[rt][0] = floatx4{kNegInf, kNegInf, kNegInf, kNegInf};
         }
+        valu_exact(0);
       }
     }
-
-    // ---- softmax over all keys of each row, then column sums ----
-    // keys past N take no part (only waves whose keys run past N look)
-    if ((cg * NT + NT) * 16 > N) {
+    // combine the 16 lanes of each row: lse = M + log2(sum_lanes l*2^(m-M));
+    // rows past R get lse = +inf and so zero probabilities
 #pragma unroll
-      for (int i = 0; i < NT; ++i)
-        if ((cg * NT + i) * 16 + li >= N) {
-#pragma unroll
-          for (int rt = 0; rt < 2; ++rt) acc[rt][i] = floatx4{kNegInf, kNegInf, kNegInf, kNegInf};
-        }
-    }
-    float M[2][4];
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        float v = acc[rt][0][q];
-#pragma unroll
-        for (int i = 1; i < NT; ++i) v = fmaxf(v, acc[rt][i][q]);
-        M[rt][q] = max16(v);
+        const float M = max16(m[rt][q]);
+        const float L = sum16(lsum[rt][q] * __builtin_amdgcn_exp2f(m[rt][q] - M));
+        const bool live = row_base + rt * 16 + gq * 4 + q < R;
+        m[rt][q] = live ? M + __builtin_amdgcn_logf(L) : kPosInf;
       }
-    if constexpr (CG > 1) {
-      if (li == 0) {
-#pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) red_max[rg][cg][rt * 16 + gq * 4 + q] = M[rt][q];
-      }
-      lds_barrier();
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          float v = red_max[rg][0][rt * 16 + gq * 4 + q];
-#pragma unroll
-          for (int o = 1; o < CG; ++o) v = fmaxf(v, red_max[rg][o][rt * 16 + gq * 4 + q]);
-          M[rt][q] = v;
-        }
-    }
-    float L[2][4];
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float mc = M[rt][q] * c;
-        float sum = 0.f;
-#pragma unroll
-        for (int i = 0; i < NT; ++i) {
-          const float e = __builtin_amdgcn_exp2f(acc[rt][i][q] * c - mc);
-          acc[rt][i][q] = e;
-          sum += e;
-        }
-        L[rt][q] = sum16(sum);
-      }
-    if constexpr (CG > 1) {
-      if (li == 0) {
-#pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) red_sum[rg][cg][rt * 16 + gq * 4 + q] = L[rt][q];
-      }
-      lds_barrier();
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          float v = red_sum[rg][0][rt * 16 + gq * 4 + q];
-#pragma unroll
-          for (int o = 1; o < CG; ++o) v += red_sum[rg][o][rt * 16 + gq * 4 + q];
-          L[rt][q] = v;
-        }
-    }
-    // softmax weight of each of this lane's eight rows (rows past R: none)
-    float wr[2][4];
-    const int row0 = rb * C::kRows + rg * 32;
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        wr[rt][q] = (row0 + rt * 16 + gq * 4 + q < R) ? __builtin_amdgcn_rcpf(L[rt][q]) : 0.f;
-    // column sums: this lane's eight rows, then the four lane groups (fixed
-    // order: (g0 + g1) + (g2 + g3)); lane group 0 adds the result to LDS
-    float* my_part = &part[rg][cg * NT * 16 + li];
-#pragma unroll
-    for (int i = 0; i < NT; ++i) {
-      float v = acc[0][i][0] * wr[0][0];
-      v = fmaf(acc[0][i][1], wr[0][1], v);
-      v = fmaf(acc[0][i][2], wr[0][2], v);
-      v = fmaf(acc[0][i][3], wr[0][3], v);
-      v = fmaf(acc[1][i][0], wr[1][0], v);
-      v = fmaf(acc[1][i][1], wr[1][1], v);
-      v = fmaf(acc[1][i][2], wr[1][2], v);
-      v = fmaf(acc[1][i][3], wr[1][3], v);
-      v += __shfl_xor(v, 16, 64);
-      v += __shfl_xor(v, 32, 64);
-      if (gq == 0) my_part[i * 16] += v;
-    }
-  }
+  };
 
-  // fixed-order reduction over the row groups
+  // ---- sweep B: probabilities exp2(x - lse); per chunk, each wave's column
+  // sums go to col_wave[chunk % 3][wave], lane group gq holding tile gq
+  auto sweep_b = [&](int ch) __attribute__((always_inline)) {
+    float v[kTps];
+#pragma unroll
+    for (int ti = 0; ti < kTps; ++ti) {
+      float sum = 0.f;
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) sum += __builtin_amdgcn_exp2f(fmaf(acc[rt][ti][q], c, -m[rt][q]));
+      v[ti] = sum;
+    }
+    // over the four lane groups, leaving lane group gq with tile gq:
+    // groups {0,1} keep tiles 0,1 and {2,3} keep tiles 2,3, then pairs split
+    const bool lo_half = gq < 2;
+    const float x0 = (lo_half ? v[0] : v[2]) + __shfl_xor(lo_half ? v[2] : v[0], 32, 64);
+    const float x1 = (lo_half ? v[1] : v[3]) + __shfl_xor(lo_half ? v[3] : v[1], 32, 64);
+    const bool odd = gq & 1;
+    const float y = (odd ? x1 : x0) + __shfl_xor(odd ? x0 : x1, 16, 64);
+    col_wave[ch % 3][wave][gq * 16 + li] = y;
+  };
+  // the eight waves' sums of one chunk, added in wave order
+  auto reduce_chunk = [&](int ch) __attribute__((always_inline)) {
+    const float* cw = &col_wave[ch % 3][0][0];
+    float sum = cw[lane];
+#pragma unroll
+    for (int w = 1; w < kScoreWaves; ++w) sum += cw[w * kChunkKeys + lane];
+    col_wg[ch * kChunkKeys + lane] = sum;
+  };
+
+  // sweep A's vector work on chunk it once its logits are formed
+  auto values_a = [&](int it) __attribute__((always_inline)) {
+    if (it == 0) {
+#pragma unroll
+      for (int ti = 0; ti < kTps; ++ti) valu_exact(ti);
+    } else {
+#pragma unroll
+      for (int ti = 0; ti < kTps; ++ti) valu_a(ti);
+    }
+  };
+
+  // The two halves of the workgroup run the same chunk sequence half a
+  // chunk apart (see below); each half is compiled as its own code path.
+  auto run = [&](auto lag_tag) __attribute__((always_inline)) {
+    constexpr bool kLag = decltype(lag_tag)::value;
+    // prologue: the first P chunks, and the offsets of the next one
+    for (int j = 0; j < P && j < n_it; ++j) {
+      read_offsets(j);
+      issue_copies(j);
+    }
+    if (P < n_it) read_offsets(P);
+
+    // Iteration it: wait for chunk it and make every wave's copies of it
+    // visible (the stage of chunk it-1 is then free and receives chunk it+P).
+    // Waves 0-3 form chunk it's logits and then do its vector work; waves 4-7,
+    // one per SIMD, first do the vector work of chunk it-1 and then form chunk
+    // it, so on every SIMD one wave keeps the matrix cores busy while the other
+    // computes exponentials.
+    auto sync = [&](int it) __attribute__((always_inline)) {
+      wait_chunks<kL, P>(min(P - 1, n_it - 1 - it));
+      lds_barrier();
+      if (it + P < n_it) {
+        issue_copies(it + P);
+        if (it + P + 1 < n_it) read_offsets(it + P + 1);
+      }
+    };
+    // (the scheduling fences keep one chunk's logits live at a time)
+    for (int it = 0; it < nch; ++it) {
+      sync(it);
+      if constexpr (!kLag) {
+        form(it);
+        __builtin_amdgcn_sched_barrier(0);
+        values_a(it);
+      } else {
+        if (it > 0) values_a(it - 1);
+        __builtin_amdgcn_sched_barrier(0);
+        form(it);
+      }
+    }
+    if constexpr (!kLag) finish_sweep_a();
+    // first chunk of sweep B: the lagging waves finish sweep A first
+    sync(nch);
+    if constexpr (!kLag) {
+      form(nch);
+      __builtin_amdgcn_sched_barrier(0);
+      sweep_b(0);
+    } else {
+      values_a(nch - 1);
+      finish_sweep_a();
+      __builtin_amdgcn_sched_barrier(0);
+      form(nch);
+    }
+    for (int it = nch + 1; it < n_it; ++it) {
+      sync(it);
+      // chunk ch's column sums were completed by both halves before this barrier
+      const int ch_done = it - nch - 2;
+      if (ch_done >= 0 && wave == ch_done % kScoreWaves) reduce_chunk(ch_done);
+      if constexpr (!kLag) {
+        form(it);
+        __builtin_amdgcn_sched_barrier(0);
+        sweep_b(it - nch);
+      } else {
+        sweep_b(it - 1 - nch);
+        __builtin_amdgcn_sched_barrier(0);
+        form(it);
+      }
+    }
+    if constexpr (kLag) sweep_b(nch - 1);
+  };
+  if (wave >= kScoreWaves / 2) run(std::true_type{});
+  else run(std::false_type{});
   lds_barrier();
-  for (int j = tid; j < N; j += kScoreThreads) {
-    float v = part[0][j];
-#pragma unroll
-    for (int p = 1; p < RG; ++p) v += part[p][j];
-    out[j] = v;
-  }
-  if (a.n_splits == 1) return;
-
-  // The last split of the unit to finish adds all splits' partial sums in
-  // split order (the order does not depend on which split finishes last).
-  __shared__ uint32_t ticket;
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) ticket = atomicAdd(&a.done[u], 1u);
-  __syncthreads();
-  if (ticket != (uint32_t)a.n_splits - 1) return;
-  __threadfence();
-  const float* slabs = a.partials + u * a.n_splits * (int64_t)N;
-  float* sc = a.scores + u * (int64_t)N;
-  for (int j = tid; j < N; j += kScoreThreads) {
-    float v = slabs[j];
-    for (int p = 1; p < a.n_splits; ++p) v += slabs[(int64_t)p * N + j];
-    sc[j] = v;
-  }
-  if (tid == 0) a.done[u] = 0;   // ready for the next call
+  for (int ch = nch - 2 > 0 ? nch - 2 : 0; ch < nch; ++ch)
+    if (wave == ch % kScoreWaves) reduce_chunk(ch);
+  lds_barrier();
+  for (int j = tid; j < N; j += kScoreThreads) out[j] = col_wg[j];
 }
 
-template <int DT, int D, int NT, int CG>
-hipError_t launch_cfg(const ScoreArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL((score_kernel<DT, D, NT, CG>), dim3((unsigned)a.n_blocks), dim3(kScoreThreads), 0,
-                     stream, a);
-  return hipGetLastError();
+// Scores of a unit: its row splits' partial column sums added in split order
+// (a kernel boundary orders them after every split's writes).
+__global__ __launch_bounds__(256) void split_sum_kernel(const float* __restrict__ partials,
+                                                        float* __restrict__ scores, int N, int n_splits) {
+  const int64_t u = blockIdx.x;
+  const int j = blockIdx.y * 256 + threadIdx.x;
+  if (j >= N) return;
+  const float* src = partials + u * n_splits * (int64_t)N + j;
+  float v = src[0];
+  for (int p = 1; p < n_splits; ++p) v += src[(int64_t)p * N];
+  scores[u * (int64_t)N + j] = v;
 }
+
+// row tiles per wave: four (512 rows per workgroup); two for fp32 with
+// 128-wide heads, whose operands take twice the registers
+int row_tiles(const Geom& g) { return (g.dtype == KARA_F32 && g.d == 128) ? 2 : 4; }
 
 template <int DT, int D>
-hipError_t launch_d(const ScoreArgs& a, const ScorePlan& sp, hipStream_t stream) {
-  if constexpr (DT == KARA_F32 && D == 128) {
-    // fp32 with 512-byte rows: at most 512 keys, at least two column groups
-    if (sp.nt == 8) return launch_cfg<DT, D, 8, 2>(a, stream);
-    return launch_cfg<DT, D, 16, 2>(a, stream);
-  } else {
-    if (sp.nt == 8) return launch_cfg<DT, D, 8, 1>(a, stream);
-    switch (sp.cg) {
-      case 1: return launch_cfg<DT, D, 16, 1>(a, stream);
-      case 2: return launch_cfg<DT, D, 16, 2>(a, stream);
-      case 4: return launch_cfg<DT, D, 16, 4>(a, stream);
-      default:
-        if constexpr (DT == KARA_BF16) return launch_cfg<DT, D, 16, 8>(a, stream);
-        return hipErrorInvalidValue;
-    }
-  }
+hipError_t launch_d(const ScoreArgs& a, hipStream_t stream) {
+  constexpr int RT = (DT == KARA_F32 && D == 128) ? 2 : 4;
+  hipLaunchKernelGGL((score_kernel<DT, D, RT>), dim3((unsigned)a.n_blocks), dim3(kScoreThreads), 0, stream, a);
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -517,32 +553,16 @@ hipError_t launch_d(const ScoreArgs& a, const ScorePlan& sp, hipStream_t stream)
 ScorePlan plan_score(const Geom& g, int64_t n_units) {
   (void)n_units;
   ScorePlan sp{};
-  const int tiles = (g.N + 15) / 16;
-  if (g.dtype == KARA_F32 && g.d == 128) {
-    sp.cg = 2;
-    sp.nt = tiles <= 16 ? 8 : 16;
-  } else if (tiles <= 8) {
-    sp.cg = 1;
-    sp.nt = 8;
-  } else {
-    sp.nt = 16;
-    sp.cg = tiles <= 16 ? 1 : tiles <= 32 ? 2 : tiles <= 64 ? 4 : 8;
-  }
-  sp.rg = kScoreWaves / sp.cg;
-  sp.n_cols = sp.cg * sp.nt * 16;
+  sp.rows_wg = kScoreWaves * 16 * row_tiles(g);
   const int64_t rows = (int64_t)g.G * g.W;
-  sp.n_rb = (int)((rows + 32 * sp.rg - 1) / (32 * sp.rg));
-  // 32 row splits per unit: the 32 CUs of one XCD work on the same unit at
-  // once, so its keys are read from that XCD's L2
-  sp.n_splits = sp.n_rb < 32 ? sp.n_rb : 32;
+  sp.n_splits = (int)((rows + sp.rows_wg - 1) / sp.rows_wg);
   return sp;
 }
-
 
 hipError_t launch_score(const Geom& g, const ScorePlan& sp, int n_layers, const void* q,
                         const PoolPtrs& k_pools, const int32_t* trig, const int32_t* block_table,
                         const int32_t* win_start, const int32_t* status, float* partials,
-                        float* scores, uint32_t* done, hipStream_t stream) {
+                        float* scores, hipStream_t stream) {
   ScoreArgs a;
   a.g = g;
   a.q = (const char*)q;
@@ -553,17 +573,17 @@ hipError_t launch_score(const Geom& g, const ScorePlan& sp, int n_layers, const 
   a.status = status;
   a.partials = partials;
   a.scores = scores;
-  a.done = done;
   a.n_splits = sp.n_splits;
-  a.n_rb = sp.n_rb;
   a.n_blocks = (int64_t)n_layers * g.n_trig * g.Hkv * sp.n_splits;
   if (a.n_blocks == 0) return hipSuccess;
-  if (g.dtype == KARA_BF16) {
-    if (g.d == 128) return launch_d<KARA_BF16, 128>(a, sp, stream);
-    return launch_d<KARA_BF16, 64>(a, sp, stream);
-  }
-  if (g.d == 128) return launch_d<KARA_F32, 128>(a, sp, stream);
-  return launch_d<KARA_F32, 64>(a, sp, stream);
+  hipError_t e;
+  if (g.dtype == KARA_BF16) e = g.d == 128 ? launch_d<KARA_BF16, 128>(a, stream) : launch_d<KARA_BF16, 64>(a, stream);
+  else e = g.d == 128 ? launch_d<KARA_F32, 128>(a, stream) : launch_d<KARA_F32, 64>(a, stream);
+  if (e != hipSuccess || sp.n_splits == 1) return e;
+  const int64_t units = a.n_blocks / sp.n_splits;
+  hipLaunchKernelGGL(split_sum_kernel, dim3((unsigned)units, (unsigned)((g.N + 255) / 256)), dim3(256), 0, stream,
+                     partials, scores, g.N, sp.n_splits);
+  return hipGetLastError();
 }
 
 }  // namespace kara
