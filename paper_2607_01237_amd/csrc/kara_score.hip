@@ -311,13 +311,14 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
   auto form = [&](int it) __attribute__((always_inline)) {
     const char* sb = kbuf + (it % S) * C::kStageBytes;
     const int ch = it < nch ? it : it - nch;
-    // one key operand at a time keeps the kernel within 256 registers; the
-    // other wave of the SIMD covers the LDS latency
+    // key operands double-buffered: the next tile's LDS reads are in flight
+    // while the matrix cores work on this one
+    Op kb[2];
+    b_read(sb, 0, kb[0]);
 #pragma unroll
     for (int ti = 0; ti < kTps; ++ti) {
-      Op kb;
-      b_read(sb, ti, kb);
-      mfma_tile(kb, ti);
+      if (ti + 1 < kTps) b_read(sb, ti + 1, kb[(ti + 1) & 1]);
+      mfma_tile(kb[ti & 1], ti);
       __builtin_amdgcn_sched_barrier(0);
     }
     if ((ch + 1) * kChunkKeys > N) {
