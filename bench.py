@@ -45,7 +45,122 @@ def parse():
     ap.add_argument("--workload", default="qwen14b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="rough budget of the CPU-oracle sample")
+    ap.add_argument("--copy-calibration-gib", type=float, default=0.0,
+                    help="run one plain streaming kernel (bf16 negation) over this many GiB before the steps, as "
+                         "the reference for rocprofv3 FETCH_SIZE / WRITE_SIZE counts")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="print the HBM-traffic summary of two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) "
+                         "of this script with --copy-calibration-gib, and exit")
     return ap.parse_args()
+
+
+# ---- HBM traffic from hardware counters ----
+# The counters come from two separate rocprofv3 --pmc runs of this script
+# (one counter block each).  Each counter is scaled by what it reads for a
+# plain streaming kernel of known size in the same run, and the result is
+# stored in profiles/ together with a hash of the kernel sources it was taken
+# on; a changed source makes the stored figure stale and the JSON reports null.
+
+TRAFFIC_SOURCES = {
+    "score": ["paper_2607_01237_amd/csrc/kara_score.hip"],
+    "select_compact": ["paper_2607_01237_amd/csrc/kara_select.hip", "paper_2607_01237_amd/csrc/kara_pages.hip"],
+}
+TRAFFIC_KERNELS = {"score": ["score_kernel", "split_sum_kernel"], "select_compact": ["compact_kernel", "select_kernel"]}
+CALIBRATION_KERNEL = "neg_kernel"
+
+
+def sources_sha256(paths):
+    import hashlib
+    h = hashlib.sha256()
+    for rel in paths:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def traffic_path(workload):
+    return os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.md")
+
+
+def load_traffic(workload):
+    """Stored per-launch HBM bytes of each stage, or None where stale/absent."""
+    out = {"score": None, "select_compact": None}
+    path = traffic_path(workload)
+    if not os.path.exists(path):
+        return out
+    text = open(path).read()
+    if "```json" not in text:
+        return out
+    blob = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+    for stage in out:
+        rec = blob.get(stage)
+        if rec and rec.get("sources_sha256") == sources_sha256(TRAFFIC_SOURCES[stage]):
+            out[stage] = rec["hbm_bytes_per_launch"]
+    return out
+
+
+def _pmc_per_dispatch(csv_path, counter):
+    import csv
+    per = {}
+    names = {}
+    for r in csv.DictReader(open(csv_path)):
+        if r["Counter_Name"] != counter:
+            continue
+        d = r["Dispatch_Id"]
+        per[d] = per.get(d, 0.0) + float(r["Counter_Value"])
+        names[d] = r["Kernel_Name"]
+    return per, names
+
+
+def summarize_pmc(fetch_csv, write_csv, workload, calib_gib):
+    fetch, names = _pmc_per_dispatch(fetch_csv, "FETCH_SIZE")
+    write, wnames = _pmc_per_dispatch(write_csv, "WRITE_SIZE")
+    true_bytes = calib_gib * 2**30
+
+    def per_kernel(per, nm, key):
+        vals = [v * 1024.0 for d, v in per.items() if key in nm[d]]   # counters are KiB per dispatch
+        return float(np.median(vals)) if vals else None, len(vals)
+
+    cf, _ = per_kernel(fetch, names, CALIBRATION_KERNEL)
+    cw, _ = per_kernel(write, wnames, CALIBRATION_KERNEL)
+    if not cf or not cw:
+        raise SystemExit("the calibration kernel is missing from the counter runs (use --copy-calibration-gib)")
+    sf, sw = true_bytes / cf, true_bytes / cw
+    lines = [f"# HBM traffic from rocprofv3 counters: {workload} workload", "",
+             "Two counter runs of the same command, one per counter block:", "", "```",
+             f"cd /tmp && export TMPDIR=/tmp && rocprofv3 --pmc FETCH_SIZE -d $REPO/gpurun_out/pmc_fetch -o pmc "
+             f"--output-format csv -- python3 $REPO/bench.py --workload {workload} --steps 1 --warmup 0 "
+             f"--no-cpu-baseline --copy-calibration-gib {calib_gib:g}",
+             "(the same with --pmc WRITE_SIZE and -d $REPO/gpurun_out/pmc_write)",
+             f"python3 bench.py --workload {workload} --copy-calibration-gib {calib_gib:g} "
+             "--summarize-pmc <fetch csv> <write csv>", "```", "",
+             f"Calibration: one bf16 negation over {calib_gib:g} GiB reads and writes {true_bytes / 1e9:.3f} GB; the "
+             f"counters read {cf / 1e9:.3f} GB fetched and {cw / 1e9:.3f} GB written, so FETCH_SIZE is scaled by "
+             f"{sf:.4f} and WRITE_SIZE by {sw:.4f}.", "",
+             "| kernel | dispatches | FETCH (GB, scaled) | WRITE (GB, scaled) |", "|---|---|---|---|"]
+    def total_of(per, nm, key):
+        vals = [v * 1024.0 for d, v in per.items() if key in nm[d]]
+        return float(np.sum(vals)), len(vals)
+
+    blob = {"workload": workload, "calibration_gib": calib_gib, "fetch_scale": sf, "write_scale": sw}
+    for stage, kernels in TRAFFIC_KERNELS.items():
+        total = 0.0
+        passes = None
+        for k in kernels:
+            f_b, n = total_of(fetch, names, k)
+            w_b, _ = total_of(write, wnames, k)
+            if n == 0:
+                continue
+            passes = n if passes is None else passes
+            lines.append(f"| {k} | {n} | {f_b * sf / n / 1e9:.3f} | {w_b * sw / n / 1e9:.3f} |")
+            total += f_b * sf + w_b * sw
+        # per pass of the stage: the first kernel of the stage runs once per pass
+        blob[stage] = {"kernels": kernels, "hbm_bytes_per_launch": total / passes if passes else None,
+                       "sources_sha256": sources_sha256(TRAFFIC_SOURCES[stage])}
+    lines += ["", "The table gives the average per dispatch.  Per pass of a stage (one scoring launch; one "
+              "selection-and-compaction pass, where the bench's staged pass runs selection as two launches and "
+              "the fused step as one):", "", "```json", json.dumps(blob, indent=1), "```"]
+    return "\n".join(lines)
 
 
 def log(msg):
@@ -155,6 +270,10 @@ def host_units(geom, p, q, kp, vp, units):
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        print(summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.workload,
+                            args.copy_calibration_gib or 1.0))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 (multi-GPU sharding is "
                                    "described in DESIGN.md and not built)"}))
@@ -195,6 +314,15 @@ def main():
         restore()
         kara.compress_window(params, meta["trig"], q, kp, vp, meta["bt"], meta["seq_lens"], meta["win_start"], True,
                              status, ws, kept=kept, freed=freed, n_freed=n_freed, stream=stream)
+
+    if args.copy_calibration_gib > 0:
+        n = int(args.copy_calibration_gib * 2**30) // 2
+        src = torch.ones(n, dtype=torch.bfloat16, device=device)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     for _ in range(args.warmup):
         step()
@@ -260,6 +388,7 @@ def main():
 
     ms = wall * 1e3 / args.steps
     win_tokens = nt * W
+    traffic = load_traffic(args.workload)
     result = {
         "metric": "window tokens compressed/s (score+select+compact); % MFMA peak / % HBM GB/s",
         "value": win_tokens / (ms * 1e-3),
@@ -283,11 +412,11 @@ def main():
         "roofline": {
             "kernel": "score_kernel (window scoring, Eq. 4)",
             "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s", "frac": ach / peak,
-            "traffic": None, "flop_per_launch": flops, "avg_launch_ms": avg["score"],
+            "traffic": traffic["score"], "flop_per_launch": flops, "avg_launch_ms": avg["score"],
         },
         "roofline_select_compact": {
             "bound": "hbm", "achieved": sc_gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": sc_gbs / PEAK_HBM_GBS,
-            "bytes_per_step": compact_bytes + select_bytes, "avg_ms": sc_ms,
+            "bytes_per_step": compact_bytes + select_bytes, "avg_ms": sc_ms, "traffic": traffic["select_compact"],
         },
         "stage_ms": avg,
         "layer_window_tokens_per_s": win_tokens * L / (ms * 1e-3),

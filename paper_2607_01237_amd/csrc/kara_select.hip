@@ -1,26 +1,40 @@
 // Per-unit selection on chip: discrete TopK (Eq. (5)), Token2Chunk
 // (Eq. (6)-(8)) and the fill rule of App. C.3.  One workgroup per
-// (sequence, layer, KV head); the unit's scores live in LDS, every ranking is
-// an exact block-wide radix select on order-preserving integer keys with
-// ties resolved by position, so the result is deterministic and independent
-// of thread scheduling.
+// (sequence, layer, KV head); the unit's scores live in LDS.  Every ranking
+// is exact and deterministic -- larger key first, lower position first among
+// equal keys -- on order-preserving integer keys: a block-wide radix select
+// for large counts, argmax rounds for the few chunks and fill positions
+// usually asked for.
 #include "kara_internal.h"
 
 namespace kara {
 namespace {
 
 constexpr int kSelThreads = 256;
-constexpr int kSelEpt = KARA_MAX_COMPRESSIBLE / kSelThreads;  // positions per thread
+constexpr int kSelEpt = KARA_MAX_COMPRESSIBLE / kSelThreads;  // positions per thread, at most
 constexpr int kSelWaves = kSelThreads / 64;
+constexpr uint32_t kArgmaxMax = 8;   // selections of at most this many items use argmax rounds
 
-struct SelSmem {
-  float a[KARA_MAX_COMPRESSIBLE];
-  int32_t disc[KARA_MAX_COMPRESSIBLE];
-  uint8_t mark[KARA_MAX_COMPRESSIBLE];  // bit0 discrete, bit1 chunk interior, bit2 fill
-  uint32_t hist[256];
+// Fixed part of the LDS; the unit's arrays follow it, sized by N.
+struct SelFixed {
+  uint32_t hist[kSelWaves][256];     // one radix histogram per wave (less atomic contention)
   uint32_t wsum[kSelWaves];
   uint32_t bc[2];
+  uint64_t best_key[2][kSelWaves];   // argmax rounds: per-wave best, double-buffered
+  int32_t best_pos[2][kSelWaves];
 };
+
+struct SelSmem {
+  SelFixed* f;
+  float* a;          // [N] scores
+  int32_t* disc;     // [N] discrete positions, ascending
+  uint8_t* mark;     // [N] bit0 discrete, bit1 chunk interior, bit2 fill
+};
+
+__host__ __device__ constexpr size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
+__host__ __device__ inline size_t sel_lds_bytes(int N) {
+  return align16(sizeof(SelFixed)) + align16((size_t)N * 4) * 2 + align16((size_t)N);
+}
 
 // Order-preserving maps to unsigned keys (larger value -> larger key); -0
 // ranks equal to +0, as in a floating-point comparison.
@@ -55,15 +69,15 @@ __device__ inline uint32_t wave_incl_scan(uint32_t v) {
 }
 
 // Exclusive prefix sum over threads in index order; *total = block sum.
-__device__ uint32_t block_excl_scan(uint32_t v, SelSmem& sm, uint32_t* total) {
+__device__ uint32_t block_excl_scan(uint32_t v, SelFixed& f, uint32_t* total) {
   const uint32_t inc = wave_incl_scan(v);
   const int w = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 63) sm.wsum[w] = inc;
+  if ((threadIdx.x & 63) == 63) f.wsum[w] = inc;
   __syncthreads();
   uint32_t off = 0, tot = 0;
 #pragma unroll
   for (int i = 0; i < kSelWaves; ++i) {
-    const uint32_t x = sm.wsum[i];
+    const uint32_t x = f.wsum[i];
     off += (i < w) ? x : 0u;
     tot += x;
   }
@@ -77,49 +91,56 @@ __device__ uint32_t block_excl_scan(uint32_t v, SelSmem& sm, uint32_t* total) {
 // [i*ept, i*ept+ept).  MSB-first radix select over 8-bit digits finds the
 // K-th key; items equal to it are then taken in position order.
 template <typename KeyT>
-__device__ void select_top(const KeyT (&key)[kSelEpt], const bool (&elig)[kSelEpt],
-                           bool (&sel)[kSelEpt], uint32_t K, SelSmem& sm) {
+__device__ void radix_top(const KeyT (&key)[kSelEpt], const bool (&elig)[kSelEpt], bool (&sel)[kSelEpt],
+                          uint32_t K, SelFixed& f) {
   constexpr int kBits = sizeof(KeyT) * 8;
-  uint32_t cnt = 0;
-#pragma unroll
-  for (int e = 0; e < kSelEpt; ++e) cnt += elig[e] ? 1u : 0u;
-  uint32_t n_el;
-  block_excl_scan(cnt, sm, &n_el);
-  if (K >= n_el || K == 0) {
-#pragma unroll
-    for (int e = 0; e < kSelEpt; ++e) sel[e] = K != 0 && elig[e];
-    return;
-  }
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6;
   KeyT prefix = 0;
   uint32_t remaining = K;
   for (int shift = kBits - 8; shift >= 0; shift -= 8) {
-    sm.hist[threadIdx.x] = 0;
+#pragma unroll
+    for (int w = 0; w < kSelWaves; ++w) f.hist[w][tid] = 0;
     __syncthreads();
+    // a thread's positions often share a digit (the top digits of nearby
+    // scores): add runs of equal digits with one atomic
+    uint32_t run_bin = 0, run = 0;
 #pragma unroll
     for (int e = 0; e < kSelEpt; ++e) {
       if (!elig[e]) continue;
       const bool match = (shift == kBits - 8) || (((key[e] ^ prefix) >> (shift + 8)) == 0);
-      if (match) atomicAdd(&sm.hist[(uint32_t)(key[e] >> shift) & 255u], 1u);
+      if (!match) continue;
+      const uint32_t b = (uint32_t)(key[e] >> shift) & 255u;
+      if (run && b == run_bin) {
+        ++run;
+      } else {
+        if (run) atomicAdd(&f.hist[wave][run_bin], run);
+        run_bin = b;
+        run = 1;
+      }
     }
+    if (run) atomicAdd(&f.hist[wave][run_bin], run);
     __syncthreads();
-    const uint32_t b = 255u - threadIdx.x;   // thread i looks at bin 255-i
-    const uint32_t h = sm.hist[b];
+    const uint32_t b = 255u - tid;   // thread i looks at bin 255-i
+    uint32_t h = 0;
+#pragma unroll
+    for (int w = 0; w < kSelWaves; ++w) h += f.hist[w][b];
     uint32_t tot;
-    const uint32_t above = block_excl_scan(h, sm, &tot);   // items in bins > b
+    const uint32_t above = block_excl_scan(h, f, &tot);   // items in bins > b
     if (above < remaining && above + h >= remaining) {
-      sm.bc[0] = b;
-      sm.bc[1] = remaining - above;
+      f.bc[0] = b;
+      f.bc[1] = remaining - above;
     }
     __syncthreads();
-    prefix |= (KeyT)sm.bc[0] << shift;
-    remaining = sm.bc[1];
+    prefix |= (KeyT)f.bc[0] << shift;
+    remaining = f.bc[1];
     __syncthreads();
   }
   uint32_t eq = 0;
 #pragma unroll
   for (int e = 0; e < kSelEpt; ++e) eq += (elig[e] && key[e] == prefix) ? 1u : 0u;
   uint32_t tot;
-  uint32_t rank = block_excl_scan(eq, sm, &tot);
+  uint32_t rank = block_excl_scan(eq, f, &tot);
 #pragma unroll
   for (int e = 0; e < kSelEpt; ++e) {
     const bool is_eq = elig[e] && key[e] == prefix;
@@ -128,12 +149,94 @@ __device__ void select_top(const KeyT (&key)[kSelEpt], const bool (&elig)[kSelEp
   }
 }
 
+// (key, pos) ordering of the rankings: a beats b
+__device__ inline bool beats(uint64_t ka, int pa, uint64_t kb, int pb) {
+  return ka > kb || (ka == kb && pa < pb);
+}
+
+// The same selection as radix_top for small K: K rounds, each taking the best
+// remaining item (a block argmax over (key desc, position asc)).
+template <typename KeyT>
+__device__ void argmax_top(const KeyT (&key)[kSelEpt], const bool (&elig)[kSelEpt], bool (&sel)[kSelEpt],
+                           uint32_t K, int base, SelFixed& f) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+#pragma unroll
+  for (int e = 0; e < kSelEpt; ++e) sel[e] = false;
+  for (uint32_t r = 0; r < K; ++r) {
+    // this thread's best: positions ascend with e, so the first maximum wins ties
+    uint64_t bk = 0;
+    int bp = 0x7fffffff;
+#pragma unroll
+    for (int e = 0; e < kSelEpt; ++e)
+      if (elig[e] && !sel[e] && beats((uint64_t)key[e], base + e, bk, bp)) {
+        bk = (uint64_t)key[e];
+        bp = base + e;
+      }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const uint32_t lo = __shfl_xor((uint32_t)bk, o, 64), hi = __shfl_xor((uint32_t)(bk >> 32), o, 64);
+      const uint64_t ok = ((uint64_t)hi << 32) | lo;
+      const int op = __shfl_xor(bp, o, 64);
+      if (beats(ok, op, bk, bp)) {
+        bk = ok;
+        bp = op;
+      }
+    }
+    const int slot = r & 1;
+    if (lane == 0) {
+      f.best_key[slot][wave] = bk;
+      f.best_pos[slot][wave] = bp;
+    }
+    __syncthreads();   // the other slot is rewritten only after the next round's barrier
+    uint64_t gk = f.best_key[slot][0];
+    int gp = f.best_pos[slot][0];
+#pragma unroll
+    for (int w = 1; w < kSelWaves; ++w)
+      if (beats(f.best_key[slot][w], f.best_pos[slot][w], gk, gp)) {
+        gk = f.best_key[slot][w];
+        gp = f.best_pos[slot][w];
+      }
+    if (gp == 0x7fffffff) break;   // nothing eligible is left
+    // only the owner marks it (other threads' slots past their own positions
+    // are never eligible)
+    const int e = gp - base;
+#pragma unroll
+    for (int i = 0; i < kSelEpt; ++i)
+      if (i == e && elig[i]) sel[i] = true;
+  }
+}
+
+template <typename KeyT>
+__device__ void select_top(const KeyT (&key)[kSelEpt], const bool (&elig)[kSelEpt], bool (&sel)[kSelEpt],
+                           uint32_t K, int base, SelFixed& f) {
+  uint32_t cnt = 0;
+#pragma unroll
+  for (int e = 0; e < kSelEpt; ++e) cnt += elig[e] ? 1u : 0u;
+  uint32_t n_el;
+  block_excl_scan(cnt, f, &n_el);
+  if (K >= n_el || K == 0) {
+#pragma unroll
+    for (int e = 0; e < kSelEpt; ++e) sel[e] = K != 0 && elig[e];
+    return;
+  }
+  if (K <= kArgmaxMax) argmax_top(key, elig, sel, K, base, f);
+  else radix_top(key, elig, sel, K, f);
+}
+
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
     Geom g, int mode, const float* __restrict__ scores, const int32_t* __restrict__ disc_in,
     int32_t* __restrict__ disc_out, int32_t* __restrict__ kept_out) {
-  __shared__ SelSmem sm;
-  const int64_t u = blockIdx.x;
+  extern __shared__ __attribute__((aligned(16))) char sel_lds[];
   const int N = g.N;
+  SelSmem sm;
+  sm.f = (SelFixed*)sel_lds;
+  sm.a = (float*)(sel_lds + align16(sizeof(SelFixed)));
+  sm.disc = (int32_t*)((char*)sm.a + align16((size_t)N * 4));
+  sm.mark = (uint8_t*)((char*)sm.disc + align16((size_t)N * 4));
+  SelFixed& f = *sm.f;
+
+  const int64_t u = blockIdx.x;
   const int tid = threadIdx.x;
   const int k = g.k_disc;
 
@@ -156,12 +259,12 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
       elig[e] = e < ept && j < N;
       key[e] = elig[e] ? ord32(sm.a[j]) : 0u;
     }
-    select_top(key, elig, sel, (uint32_t)k, sm);
+    select_top(key, elig, sel, (uint32_t)k, base, f);
     uint32_t c = 0;
 #pragma unroll
     for (int e = 0; e < kSelEpt; ++e) c += sel[e] ? 1u : 0u;
     uint32_t tot;
-    uint32_t r = block_excl_scan(c, sm, &tot);
+    uint32_t r = block_excl_scan(c, f, &tot);
 #pragma unroll
     for (int e = 0; e < kSelEpt; ++e)
       if (sel[e]) {
@@ -214,7 +317,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
         }
       }
     }
-    select_top(key2, el2, s2, (uint32_t)g.n_chunks, sm);
+    select_top(key2, el2, s2, (uint32_t)g.n_chunks, base2, f);
 #pragma unroll
     for (int e = 0; e < kSelEpt; ++e)
       if (s2[e]) {
@@ -225,7 +328,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
       }
   }
   uint32_t added;
-  block_excl_scan(added_here, sm, &added);
+  block_excl_scan(added_here, f, &added);
 
   // App. C.3: top up to alpha added positions with the best unselected ones
   const int fill = g.alpha - (int)added;
@@ -236,7 +339,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
       elig[e] = e < ept && j < N && sm.mark[j] == 0;
       key[e] = elig[e] ? ord32(sm.a[j]) : 0u;
     }
-    select_top(key, elig, sel, (uint32_t)fill, sm);
+    select_top(key, elig, sel, (uint32_t)fill, base, f);
 #pragma unroll
     for (int e = 0; e < kSelEpt; ++e)
       if (sel[e]) sm.mark[base + e] |= 4;
@@ -251,7 +354,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     if (e < ept && j < N && sm.mark[j]) ++c;
   }
   uint32_t tot;
-  uint32_t r = block_excl_scan(c, sm, &tot);
+  uint32_t r = block_excl_scan(c, f, &tot);
 #pragma unroll
   for (int e = 0; e < kSelEpt; ++e) {
     const int j = base + e;
@@ -265,10 +368,9 @@ hipError_t launch_select(const Geom& g, int64_t n_units, int mode, const float* 
                          const int32_t* discrete_in, int32_t* discrete_out, int32_t* kept_out,
                          hipStream_t stream) {
   if (n_units <= 0) return hipSuccess;
-  hipLaunchKernelGGL(select_kernel, dim3((unsigned)n_units), dim3(kSelThreads), 0, stream, g, mode, scores,
-                     discrete_in, discrete_out, kept_out);
+  hipLaunchKernelGGL(select_kernel, dim3((unsigned)n_units), dim3(kSelThreads), sel_lds_bytes(g.N), stream, g,
+                     mode, scores, discrete_in, discrete_out, kept_out);
   return hipGetLastError();
 }
-
 
 }  // namespace kara
