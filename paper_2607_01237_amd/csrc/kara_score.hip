@@ -75,7 +75,8 @@ struct Cfg {
   static constexpr int kRowsWG = kScoreWaves * 16 * RT;  // query rows per workgroup
   static constexpr int kStageBytes = kChunkKeys * kRowBytes;
   static constexpr int kL = kStageBytes / (kScoreThreads * 16);   // copies per thread per chunk
-  static constexpr int kFixedBytes = 2 * kMaxChunks * kChunkKeys * 4 + 2 * kScoreWaves * kChunkKeys * 4;
+  // key offsets and workgroup column sums, plus up to five chunks' per-wave column sums
+  static constexpr int kFixedBytes = 2 * kMaxChunks * kChunkKeys * 4 + 5 * kScoreWaves * kChunkKeys * 4;
   static constexpr int fit_stages() {
     int s = 6;
     while (s > 2 && s * kStageBytes + kFixedBytes > kLdsLimit) --s;
@@ -180,7 +181,14 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
   using Op = Operand<DT, D>;
   constexpr int CPR = C::kCPR;
   constexpr int S = C::kStages;
-  constexpr int P = S - 1;                // prefetch distance in chunks
+  // The ring is synchronised once per group of GS chunks (two when there
+  // are stages enough): one barrier then covers two chunks of work.  Chunks
+  // are copied P ahead of the group being worked on.
+  constexpr int GS = S >= 5 ? 2 : 1;
+  constexpr int P = S - GS;
+  // a chunk's per-wave column sums are added at the first group start after
+  // both halves wrote them, at most 1 + 2*GS chunks later
+  constexpr int kColSlots = 1 + 2 * GS;
   constexpr int kL = C::kL;
   constexpr int KC = Op::kChunks;
   static_assert(P <= 6, "wait_chunks covers at most six chunks in flight");
@@ -189,9 +197,9 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
   // byte offset / 16 of every compressible key row in the K pool (the block
   // table resolved once per workgroup); padding entries repeat key 0
   __shared__ uint32_t key_off[kMaxChunks * kChunkKeys];
-  // this workgroup's column sums; per-wave column sums of the last three chunks
+  // this workgroup's column sums; per-wave column sums of the last kColSlots chunks
   __shared__ float col_wg[kMaxChunks * kChunkKeys];
-  __shared__ float col_wave[3][kScoreWaves][kChunkKeys];
+  __shared__ float col_wave[kColSlots][kScoreWaves][kChunkKeys];
 
   const Geom& g = a.g;
   const int tid = threadIdx.x;
@@ -276,16 +284,17 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
     kr0[r] = kr;
   }
   const int n_it = 2 * nch;                // sweep A, then sweep B, over the same chunks
-  uint32_t coff[kL];
-  auto read_offsets = [&](int it) __attribute__((always_inline)) {
+  uint32_t coff[GS][kL];   // key offsets of the next group's copies
+  auto read_offsets = [&](int it, int x) __attribute__((always_inline)) {
     const int ch = it < nch ? it : it - nch;
 #pragma unroll
-    for (int r = 0; r < kL; ++r) coff[r] = key_off[ch * kChunkKeys + kr0[r]];
+    for (int r = 0; r < kL; ++r) coff[x][r] = key_off[ch * kChunkKeys + kr0[r]];
   };
-  auto issue_copies = [&](int it) __attribute__((always_inline)) {
+  auto issue_copies = [&](int it, int x) __attribute__((always_inline)) {
     char* sbase = kbuf + (it % S) * C::kStageBytes;
 #pragma unroll
-    for (int r = 0; r < kL; ++r) copy16(kpool_c[r] + (uint64_t)coff[r] * 16, sbase + (r * kScoreWaves + wave) * 1024);
+    for (int r = 0; r < kL; ++r)
+      copy16(kpool_c[r] + (uint64_t)coff[x][r] * 16, sbase + (r * kScoreWaves + wave) * 1024);
   };
 
   // per-lane LDS byte offsets of the key operand chunks (key rows are
@@ -407,7 +416,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
   };
 
   // ---- sweep B: probabilities exp2(x - lse); per chunk, each wave's column
-  // sums go to col_wave[chunk % 3][wave], lane group gq holding tile gq
+  // sums go to col_wave[chunk % kColSlots][wave], lane group gq holding tile gq
   auto sweep_b = [&](int ch) __attribute__((always_inline)) {
     float v[kTps];
 #pragma unroll
@@ -426,11 +435,11 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
     const float x1 = (lo_half ? v[1] : v[3]) + __shfl_xor(lo_half ? v[3] : v[1], 32, 64);
     const bool odd = gq & 1;
     const float y = (odd ? x1 : x0) + __shfl_xor(odd ? x0 : x1, 16, 64);
-    col_wave[ch % 3][wave][gq * 16 + li] = y;
+    col_wave[ch % kColSlots][wave][gq * 16 + li] = y;
   };
   // the eight waves' sums of one chunk, added in wave order
   auto reduce_chunk = [&](int ch) __attribute__((always_inline)) {
-    const float* cw = &col_wave[ch % 3][0][0];
+    const float* cw = &col_wave[ch % kColSlots][0][0];
     float sum = cw[lane];
 #pragma unroll
     for (int w = 1; w < kScoreWaves; ++w) sum += cw[w * kChunkKeys + lane];
@@ -452,12 +461,14 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
   // chunk apart (see below); each half is compiled as its own code path.
   auto run = [&](auto lag_tag) __attribute__((always_inline)) {
     constexpr bool kLag = decltype(lag_tag)::value;
-    // prologue: the first P chunks, and the offsets of the next one
+    // prologue: the first P chunks, and the offsets of the next group's
     for (int j = 0; j < P && j < n_it; ++j) {
-      read_offsets(j);
-      issue_copies(j);
+      read_offsets(j, 0);
+      issue_copies(j, 0);
     }
-    if (P < n_it) read_offsets(P);
+#pragma unroll
+    for (int x = 0; x < GS; ++x)
+      if (P + x < n_it) read_offsets(P + x, x);
 
     // Iteration it: wait for chunk it and make every wave's copies of it
     // visible (the stage of chunk it-1 is then free and receives chunk it+P).
@@ -465,13 +476,19 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
     // one per SIMD, first do the vector work of chunk it-1 and then form chunk
     // it, so on every SIMD one wave keeps the matrix cores busy while the other
     // computes exponentials.
+    // At the start of each group (it a multiple of GS; n_it is even): wait
+    // for the group's chunks and make every wave's copies of them visible;
+    // the previous group's stages are then free and receive chunks it+P...
     auto sync = [&](int it) __attribute__((always_inline)) {
-      wait_chunks<kL, P>(min(P - 1, n_it - 1 - it));
+      if (it % GS != 0) return;
+      wait_chunks<kL, P>(min(P - GS, n_it - GS - it));
       lds_barrier();
-      if (it + P < n_it) {
-        issue_copies(it + P);
-        if (it + P + 1 < n_it) read_offsets(it + P + 1);
-      }
+#pragma unroll
+      for (int x = 0; x < GS; ++x)
+        if (it + P + x < n_it) issue_copies(it + P + x, x);
+#pragma unroll
+      for (int x = 0; x < GS; ++x)
+        if (it + GS + P + x < n_it) read_offsets(it + GS + P + x, x);
     };
     // (the scheduling fences keep one chunk's logits live at a time)
     for (int it = 0; it < nch; ++it) {
@@ -501,9 +518,15 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
     }
     for (int it = nch + 1; it < n_it; ++it) {
       sync(it);
-      // chunk ch's column sums were completed by both halves before this barrier
-      const int ch_done = it - nch - 2;
-      if (ch_done >= 0 && wave == ch_done % kScoreWaves) reduce_chunk(ch_done);
+      // at a group start: chunks whose column sums both halves completed
+      // before this group's barrier (chunk ch: at iterations nch+ch, nch+ch+1)
+      if (it % GS == 0) {
+#pragma unroll
+        for (int x = 0; x < GS; ++x) {
+          const int ch = it - nch - 1 - GS + x;
+          if (ch >= 0 && wave == ch % kScoreWaves) reduce_chunk(ch);
+        }
+      }
       if constexpr (!kLag) {
         form(it);
         __builtin_amdgcn_sched_barrier(0);
@@ -519,7 +542,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
   if (wave >= kScoreWaves / 2) run(std::true_type{});
   else run(std::false_type{});
   lds_barrier();
-  for (int ch = nch - 2 > 0 ? nch - 2 : 0; ch < nch; ++ch)
+  for (int ch = nch - GS - 1 > 0 ? nch - GS - 1 : 0; ch < nch; ++ch)
     if (wave == ch % kScoreWaves) reduce_chunk(ch);
   lds_barrier();
   for (int j = tid; j < N; j += kScoreThreads) out[j] = col_wg[j];

@@ -66,6 +66,17 @@ def test_odd_geometry_and_flags():
     _run(cfg, trig=[0, 1, 2, 3, 4, 2], seq_lens=lens)
 
 
+@pytest.mark.parametrize("window,head_dim", [(40, 128), (150, 128), (330, 128), (150, 64), (1000, 64)])
+def test_chunk_counts(window, head_dim):
+    # 64-key chunks: one (N=40), odd counts whose last chunk is partial
+    # (150 -> 3, 1000 -> 16 with d=64), and 330 -> 6 with a 10-key tail;
+    # G*W not a multiple of the 512 rows of a workgroup
+    budget = max(2, (window + 4) // 5)
+    cfg = ki.workload("batch8", n_seqs=2, n_layers=1, window=window, budget=budget, chunk_budget=min(4, budget - 1),
+                      max_chunk_len=4, head_dim=head_dim, prefix=(0, 70), tail=(0, 12), num_pages=256)
+    _run(cfg)
+
+
 def test_fp32_head128_mha():
     cfg = ki.workload("tiny", n_seqs=3, n_q_heads=2, n_kv_heads=2, head_dim=128, window=96, budget=20,
                       chunk_budget=6, max_chunk_len=5, num_pages=64, prefix=(3, 40), tail=(0, 9))
