@@ -17,6 +17,12 @@ the HBM-bound stages.  `cpu_baseline` times the CPU oracle on a bounded
 sample of units on this host.
 
     python bench.py [--steps K] [--warmup W] [--workload qwen14b|batch8|ragged|tiny]
+    python bench.py --workload soak [--intervals n] [--warmup W]
+
+The soak runs the compression step inside a decode loop (append, decode
+attention, compress, reclaim pages; paper_2607_01237_amd/soak.py) and reports
+per-event compression latency, per-step decode latency and pages reclaimed;
+its `value` averages the events after the first W.
 """
 
 from __future__ import annotations
@@ -44,6 +50,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="qwen14b")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--intervals", type=int, default=0, help="soak only: number of compression intervals "
+                                                             "(default: the workload's 31)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="rough budget of the CPU-oracle sample")
     ap.add_argument("--copy-calibration-gib", type=float, default=0.0,
                     help="run one plain streaming kernel (bf16 negation) over this many GiB before the steps, as "
@@ -268,6 +276,113 @@ def host_units(geom, p, q, kp, vp, units):
     return out_q, out_k, out_v
 
 
+def run_soak(args):
+    """The decode-loop soak: intervals of appends and decode steps, each
+    ending in one timed compression event over every sequence and layer."""
+    import torch
+
+    import kara_inputs as ki
+    from paper_2607_01237_amd import kara
+    from paper_2607_01237_amd.soak import Soak
+
+    kara.load()
+    device = torch.device("cuda:0")
+    torch.cuda.set_device(device)
+    cfg = ki.workload("soak")
+    if args.intervals:
+        cfg["n_intervals"] = args.intervals
+    geom = ki.soak_geometry(cfg)
+    gen = torch.Generator(device=device)
+    gen.manual_seed(cfg["seed"])
+    sk = Soak(cfg, geom, device, gen)
+    log(f"soak: {sk.n} sequences x {sk.L} layers, {cfg['n_intervals']} intervals, pool {geom.num_pages} pages "
+        f"({geom.num_pages * sk.page_bytes() / 1e9:.1f} GB K+V), mem {torch.cuda.memory_allocated() / 2**30:.1f} GiB")
+    sk.prompt()
+    torch.cuda.synchronize()
+    n_int = cfg["n_intervals"]
+    n_dec = cfg["window"] // cfg["append_chunk"]
+    p = sk.p
+    N = p["window"] - p["buffer"]
+    G = p["n_q_heads"] // p["n_kv_heads"]
+    flops = 2.0 * sk.L * sk.n * p["n_kv_heads"] * G * p["window"] * N * p["head_dim"]
+    ev = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    comp_ms, dec_ms, reclaimed, resident, logical = [], [], [], [], []
+    score_ms = []
+    t0 = time.perf_counter()
+    for i in range(n_int):
+        dec = []
+        for _ in range(n_dec):
+            sk.append(cfg["append_chunk"])
+            e = ev()
+            sk.decode(e)
+            dec.append(e)
+        if i >= n_int - 3:
+            # the scoring kernel alone on this event's inputs (reads only)
+            sk.q.normal_(generator=gen)
+            sk.win_start.copy_(torch.from_numpy(sk.p0))
+            e = ev()
+            e[0].record()
+            kara.score_window(sk.params, sk.seqs, sk.q, sk.kp, sk.bt, sk.lens, sk.win_start, sk.scores, sk.status,
+                              sk.ws)
+            e[1].record()
+            torch.cuda.synchronize()
+            score_ms.append(e[0].elapsed_time(e[1]))
+        ce = ev()
+        sk.compress(ce)
+        got = sk.settle()
+        comp_ms.append(ce[0].elapsed_time(ce[1]))
+        dec_ms.append([a.elapsed_time(b) for a, b in dec])
+        reclaimed.append(got)
+        mapped = int((sk.pool.table >= 0).sum())
+        resident.append(mapped)
+        logical.append(cfg["prefix"][0] + (i + 1) * cfg["window"])
+        log(f"event {i + 1}/{n_int}: compress {comp_ms[-1]:.2f} ms, decode {np.mean(dec_ms[-1]):.2f} ms/step, "
+            f"reclaimed {got} pages, resident {mapped * sk.page_bytes() / 1e9:.1f} GB, "
+            f"{time.perf_counter() - t0:.0f} s")
+    timed = comp_ms[args.warmup:] if len(comp_ms) > args.warmup else comp_ms
+    ms = float(np.mean(timed))
+    win_tokens = sk.n * sk.W
+    tok_bytes = sk.page_bytes() // sk.bs
+    ach = flops / (np.mean(score_ms) * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if p["dtype"] == "bf16" else PEAK_F32_TFLOPS
+    result = {
+        "metric": "window tokens compressed/s (score+select+compact); % MFMA peak / % HBM GB/s",
+        "value": win_tokens / (ms * 1e-3),
+        "unit": "window tokens/s",
+        "n_gpus": 1,
+        "steps": len(timed),
+        "warmup": len(comp_ms) - len(timed),
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": p["dtype"],
+        "data": "synthetic (fresh seeded N(0,1) Q/K/V every interval; no model weights or datasets)",
+        "config": {
+            "workload": "soak", "sequences": sk.n, "layers": sk.L, "q_heads": p["n_q_heads"],
+            "kv_heads": p["n_kv_heads"], "head_dim": p["head_dim"], "window": p["window"], "budget": p["budget"],
+            "prompt": cfg["prefix"][0], "intervals": n_int, "append_chunk": cfg["append_chunk"],
+            "decode_steps_per_interval": n_dec, "pages": geom.num_pages,
+        },
+        "roofline": {
+            "kernel": "score_kernel (window scoring, Eq. 4)",
+            "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s", "frac": ach / peak, "traffic": None,
+            "flop_per_launch": flops, "avg_launch_ms": float(np.mean(score_ms)),
+        },
+        "soak": {
+            "compress_ms_per_event": comp_ms,
+            "decode_ms_per_step_mean_per_event": [float(np.mean(x)) for x in dec_ms],
+            "pages_reclaimed_per_event": reclaimed,
+            "pages_reclaimed_total": int(sum(reclaimed)),
+            "logical_tokens_per_sequence": logical,
+            "resident_GB_per_event": [r * sk.page_bytes() / 1e9 for r in resident],
+            "uncompressed_GB_at_end": sk.n * logical[-1] * tok_bytes / 1e9,
+            "decode_ms_per_step_last_interval": float(np.mean(dec_ms[-1])),
+        },
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     args = parse()
     if args.summarize_pmc:
@@ -278,6 +393,9 @@ def main():
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 (multi-GPU sharding is "
                                    "described in DESIGN.md and not built)"}))
         sys.exit(2)
+    if args.workload == "soak":
+        run_soak(args)
+        return
     import torch
 
     import kara_inputs as ki

@@ -25,8 +25,12 @@ Workloads (name -> what it is):
                 sequence's uncompressed fill drawn from 0..W+127, so only the
                 sequences with a full window trigger; pool ~90 % occupied,
                 pages handed out from a shuffled free list.
-* ``soak``      128 sequences, 40 layers, 40/8 heads; contexts grow from 1K
-                by W=1024 generated tokens between compression events.
+* ``soak``      128 sequences, 40 layers, 40/8 heads; a 1K prompt, then 31
+                intervals of W=1024 generated tokens (appended 128 at a time,
+                one decode step per append) each ending in a compression
+                event, so contexts grow to 32K logical tokens; fresh N(0,1)
+                Q/K/V every interval; pool = peak need + 1 %, pages handed out
+                from a shuffled free list (``soak_geometry``).
 
 Every workload uses U=0 unless a variant sets ``buffer``: the tiny case's
 "budget 26 of W=128 (20 %)" equals ceil(0.2*128) only with no buffer.
@@ -59,7 +63,7 @@ BASE = {
     "soak": dict(n_seqs=128, n_layers=40, n_q_heads=40, n_kv_heads=8, head_dim=128, dtype="bf16",
                  window=1024, buffer=0, budget=205, max_chunk_len=8, chunk_budget=16,
                  block_size=16, num_pages=None, seed=4, prefix=(1024, 1024), tail=(0, 0),
-                 pool_slack=0.10, key_mode="normal"),
+                 pool_slack=0.01, key_mode="normal", n_intervals=31, append_chunk=128, n_dec=8),
 }
 
 
@@ -137,6 +141,33 @@ def make_geometry(cfg: dict) -> Geometry:
                     win_start=win_start.astype(np.int32), block_table=table,
                     num_pages=num_pages, max_blocks=max_blocks,
                     extra=dict(free_pages=free_list[c:].astype(np.int32)))
+
+
+@dataclass
+class SoakGeometry:
+    """Sizes of the decode-loop soak: the longest physical length any
+    sequence reaches, the block-table width, the pool, and the initial
+    (shuffled) free list."""
+    max_tokens: int
+    max_blocks: int
+    num_pages: int
+    free_list: np.ndarray
+
+
+def soak_geometry(cfg: dict) -> SoakGeometry:
+    """Each interval appends W tokens; the event then leaves `budget` of them
+    (no buffer, U = 0), so before the last event a sequence holds
+    prompt + (n-1)*budget + W."""
+    if cfg["buffer"] != 0:
+        raise ValueError("the soak runs with U = 0")
+    bs, W = cfg["block_size"], cfg["window"]
+    prompt = cfg["prefix"][0]
+    max_tokens = prompt + (cfg["n_intervals"] - 1) * cfg["budget"] + W
+    max_blocks = _blocks(max_tokens, bs)
+    num_pages = int(np.ceil(cfg["n_seqs"] * max_blocks * (1.0 + cfg["pool_slack"])))
+    rng = np.random.default_rng(cfg["seed"])
+    return SoakGeometry(max_tokens=max_tokens, max_blocks=max_blocks, num_pages=num_pages,
+                        free_list=rng.permutation(num_pages).astype(np.int32))
 
 
 # ---------------------------------------------------------------- tensors

@@ -7,7 +7,7 @@
 
 using namespace kara;
 
-namespace {
+namespace kara {
 
 constexpr int kMaxWindow = 1 << 16;
 
@@ -58,6 +58,26 @@ kara_status_t make_geom(const kara_params_t* p, int32_t n_trig, Geom* g) {
   return KARA_OK;
 }
 
+// the last HIP error a call on this thread failed with (hipSuccess: none)
+thread_local hipError_t t_last_hip_error = hipSuccess;
+
+kara_status_t hip_status(hipError_t e) {
+  if (e == hipSuccess) return KARA_OK;
+  t_last_hip_error = e;
+  return KARA_ERR_HIP;
+}
+
+bool pools_ok(const void* const* pools, int n_layers) {
+  if (!pools) return false;
+  for (int i = 0; i < n_layers; ++i)
+    if (!pools[i]) return false;
+  return true;
+}
+
+}  // namespace kara
+
+namespace {
+
 inline size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct WsLayout {
@@ -80,14 +100,6 @@ WsLayout ws_layout(const Geom& g, int n_layers, const ScorePlan& sp) {
   return w;
 }
 
-// the last HIP error a call on this thread failed with (hipSuccess: none)
-thread_local hipError_t t_last_hip_error = hipSuccess;
-
-kara_status_t hip_status(hipError_t e) {
-  if (e == hipSuccess) return KARA_OK;
-  t_last_hip_error = e;
-  return KARA_ERR_HIP;
-}
 
 // Runs fn(layer0, count, pool-pointer structs) over chunks of at most
 // kMaxLayersPerLaunch layers.
@@ -107,12 +119,6 @@ hipError_t for_layer_chunks(int n_layers, const void* const* k_pools, const void
   return hipSuccess;
 }
 
-bool pools_ok(const void* const* pools, int n_layers) {
-  if (!pools) return false;
-  for (int i = 0; i < n_layers; ++i)
-    if (!pools[i]) return false;
-  return true;
-}
 
 // Window scores of every layer.
 hipError_t run_score(const Geom& g, const ScorePlan& sp, int n_layers, const void* q,

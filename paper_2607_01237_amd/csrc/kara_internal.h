@@ -30,14 +30,21 @@ struct PoolPtrs {
   void* p[kMaxLayersPerLaunch];
 };
 
+// Host helpers shared by the API files (kara_api.cpp): parameter checks into
+// a Geom (n_trig: the count of listed sequences), HIP status mapping that
+// remembers the error for kara_last_hip_error, pool-array check.
+kara_status_t make_geom(const kara_params_t* p, int32_t n_trig, Geom* g);
+kara_status_t hip_status(hipError_t e);
+bool pools_ok(const void* const* pools, int n_layers);
+
 // Validation kernel (kara_pages.hip).
 hipError_t launch_validate(const Geom& g, const int32_t* trig, const int32_t* block_table,
                            const int32_t* seq_lens, const int32_t* win_start, int32_t* status,
                            hipStream_t stream);
 
 // Scoring (kara_score.hip): per unit, n_splits workgroups each write a
-// partial column sum; the last to finish adds them in split order into
-// `scores` (with one split the workgroup writes `scores` directly).
+// partial column sum into `partials`, and a second kernel adds them in split
+// order into `scores` (with one split the workgroup writes `scores` directly).
 struct ScorePlan {
   int rows_wg;          // query rows per workgroup
   int n_splits;         // row splits (workgroups) per unit

@@ -14,7 +14,7 @@ import re
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libkara.so")
-HEADER = os.path.join(os.path.dirname(_PKG), "include", "kara.h")
+HEADERS = [os.path.join(os.path.dirname(_PKG), "include", h) for h in ("kara.h", "kara_harness.h")]
 
 BF16, F32 = 0, 1
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
@@ -75,15 +75,21 @@ _SIGS = {
     "kara_commit_tables": (_I32, [_PAR, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     "kara_compress_window": (_I32, [_PAR, _I32, _VP, _I32, _VP, _PP, _PP, _VP, _VP, _VP, _I32, _VP, _VP,
                                     _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP]),
+    "kara_harness_kv_append": (_I32, [_PAR, _I32, _VP, _I32, _I32, _VP, _VP, _PP, _PP, _VP, _VP, _VP, _VP]),
+    "kara_harness_decode_workspace_size": (_I32, [_PAR, _I32, _I32, _I32, ctypes.POINTER(ctypes.c_size_t)]),
+    "kara_harness_decode_attention": (_I32, [_PAR, _I32, _VP, _I32, _VP, _PP, _PP, _VP, _VP, _I32, _VP, _VP,
+                                             ctypes.c_size_t, _VP]),
 }
 
 _lib = None
 
 
 def header_functions() -> list[str]:
-    """Names of the functions include/kara.h declares."""
-    text = open(HEADER).read()
-    return sorted(set(re.findall(r"^\S.*?\b(kara_\w+)\s*\(", text, flags=re.M)))
+    """Names of the functions include/kara.h and include/kara_harness.h declare."""
+    names = set()
+    for h in HEADERS:
+        names |= set(re.findall(r"^\S.*?\b(kara_\w+)\s*\(", open(h).read(), flags=re.M))
+    return sorted(names)
 
 
 def load(path: str = LIB_PATH) -> ctypes.CDLL:
@@ -197,3 +203,29 @@ def compress_window(p, trig, q, k_pools, v_pools, block_table, seq_lens, win_sta
         _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), _ptr(win_start), int(bool(commit)),
         _ptr(scores), _ptr(discrete), _ptr(kept), _ptr(freed), _ptr(n_freed), _ptr(status), _ptr(workspace),
         workspace.numel() * workspace.element_size() if workspace is not None else 0, _stream(stream)))
+
+
+# ---- decoding-side helpers (include/kara_harness.h)
+
+def kv_append(p, seqs, k_new, v_new, k_pools, v_pools, block_table, seq_lens, status, stream=None):
+    """Appends k_new / v_new [n_layers][n][n_new][Hkv][d] after each listed sequence's tokens."""
+    _check("kara_harness_kv_append", load().kara_harness_kv_append(
+        ctypes.byref(p), seqs.numel(), _ptr(seqs), k_new.shape[2], len(k_pools), _ptr(k_new), _ptr(v_new),
+        _ptr_array(k_pools), _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), _ptr(status),
+        _stream(stream)))
+
+
+def decode_workspace_size(p, n, n_layers, max_len) -> int:
+    out = ctypes.c_size_t(0)
+    _check("kara_harness_decode_workspace_size", load().kara_harness_decode_workspace_size(
+        ctypes.byref(p), n, n_layers, max_len, ctypes.byref(out)))
+    return int(out.value)
+
+
+def decode_attention(p, seqs, q, k_pools, v_pools, block_table, seq_lens, max_len, out, workspace,
+                     stream=None):
+    """One query per (layer, sequence, query head) over the paged cache; fp32 out of q's shape."""
+    _check("kara_harness_decode_attention", load().kara_harness_decode_attention(
+        ctypes.byref(p), seqs.numel(), _ptr(seqs), len(k_pools), _ptr(q), _ptr_array(k_pools),
+        _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), max_len, _ptr(out), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream)))

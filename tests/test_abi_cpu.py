@@ -1,5 +1,5 @@
 """The C-ABI library without a GPU: it loads, exports every function
-include/kara.h declares, and its host-side argument checks reject bad calls
+include/kara.h and include/kara_harness.h declare, and its host-side argument checks reject bad calls
 before anything is launched."""
 import ctypes
 import os
@@ -29,7 +29,7 @@ def good_params(**kw):
 
 def test_exports_every_declared_function(lib):
     names = kara.header_functions()
-    assert len(names) == 11
+    assert len(names) == 14
     for n in names:
         assert hasattr(lib, n), n
 
@@ -105,3 +105,24 @@ def test_workspace_checked_before_launch(lib):
     rc = lib.kara_compress_window(ctypes.byref(p), 2, fake, 1, fake, pools, pools, fake, fake, fake, 1, None,
                                   None, None, fake, fake, fake, fake, 16, None)
     assert rc == kara.ERR_WORKSPACE
+
+
+def test_harness_checks_before_launch(lib):
+    p = good_params()
+    r = ctypes.byref(p)
+    out = ctypes.c_size_t(0)
+    assert lib.kara_harness_decode_workspace_size(r, 4, 2, 1000, ctypes.byref(out)) == kara.OK
+    # 4 sequences x 2 layers x 32 query heads x 4 splits of 256 keys x (m, l, o[128])
+    assert out.value == 4 * 2 * 32 * 4 * 130 * 4
+    # longer than the block table can hold
+    assert lib.kara_harness_decode_workspace_size(r, 4, 2, 200 * 16 + 1, ctypes.byref(out)) == kara.ERR_INVALID_ARG
+    assert lib.kara_harness_kv_append(r, 4, None, 8, 1, None, None, None, None, None, None, None, None) \
+        == kara.ERR_INVALID_ARG
+    assert lib.kara_harness_kv_append(r, 0, None, 8, 1, None, None, None, None, None, None, None, None) == kara.OK
+    fake = ctypes.c_void_p(0x1000)
+    pools = (ctypes.c_void_p * 1)(0x1000)
+    assert lib.kara_harness_decode_attention(r, 4, fake, 1, fake, pools, pools, fake, fake, 1000, fake, fake, 16,
+                                             None) == kara.ERR_WORKSPACE
+    wide = good_params(n_q_heads=256, n_kv_heads=8)
+    assert lib.kara_harness_decode_attention(ctypes.byref(wide), 4, fake, 1, fake, pools, pools, fake, fake, 1000,
+                                             fake, fake, 1 << 30, None) == kara.ERR_UNSUPPORTED
