@@ -97,3 +97,37 @@ def test_deterministic():
     b = kc.run_compress(kc.setup(cfg))
     for k in ("scores", "discrete", "kept", "bt", "seq_lens", "freed", "n_freed", "status"):
         assert np.array_equal(a[k].view(np.uint8), b[k].view(np.uint8)), k
+
+
+def test_bf16_long_window():
+    # N = 2500: 40 64-key chunks with a 4-key tail; G=2, one KV head
+    cfg = ki.workload("batch8", n_seqs=2, n_layers=1, n_q_heads=2, n_kv_heads=1, window=2500, budget=500,
+                      prefix=(0, 100), tail=(0, 5), num_pages=512, key_mode="normal")
+    _run(cfg)
+
+
+@pytest.mark.parametrize("pos,scale", [(700, 16.0), (300, 16.0), (40, 16.0), (700, -16.0)])
+def test_outlier_keys(pos, scale):
+    # One window key per (sequence, head) scaled by 16 (exact in bf16).
+    # Positive: its logits lie far above the maximum of the row's first keys,
+    # where the scoring kernel takes its reference, and it takes nearly all
+    # the probability of the rows it agrees with.  Negative: its probabilities
+    # sit tens of binades below the row maxima.
+    import kara_check as kc
+    _need_gpu()
+    cfg = ki.workload("batch8", n_seqs=2, n_layers=1, key_mode="normal")
+    print(f"\n[case] outlier key at window position {pos}, scale {scale}", flush=True)
+    case = kc.setup(cfg)
+    bs = case.p["block_size"]
+    for t, s_ in enumerate(case.geom.trig):
+        j = int(case.geom.win_start[s_]) + pos
+        page = int(case.geom.block_table[s_, j // bs])
+        case.kp[0][page, :, j % bs, :] *= scale
+    case.host = kc.snapshot(case)
+    rep, gpu = kc.full_check(case)
+    print(f"[case] ok {rep}", flush=True)
+    if scale > 0:
+        # the outlier takes nearly all the probability of the rows whose dot
+        # product with it is positive, about half of the G*W rows
+        w = gpu["scores"][0, :, :, pos]
+        assert (w > 0.25 * case.p["n_q_heads"] // case.p["n_kv_heads"] * case.p["window"]).all()
