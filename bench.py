@@ -185,7 +185,7 @@ def setup(cfg, device):
     p = geom.params()
     L, nt = cfg["n_layers"], len(geom.trig)
     dt = ki.torch_dtype(cfg)
-    q = torch.empty((L, nt, cfg["window"], cfg["n_q_heads"], cfg["head_dim"]), dtype=dt, device=device)
+    q = torch.empty((L, nt, ki.scoring_queries(cfg), cfg["n_q_heads"], cfg["head_dim"]), dtype=dt, device=device)
     kp, vp = [], []
     for l in range(L):
         q[l] = ki.make_queries(geom, l, device)
@@ -266,7 +266,7 @@ def host_units(geom, p, q, kp, vp, units):
     for (l, t, h) in units:
         s = int(geom.trig[t])
         p0 = int(geom.win_start[s])
-        rows = q[l, t, :, h * G:(h + 1) * G, :].reshape(W * G, -1)
+        rows = q[l, t, :, h * G:(h + 1) * G, :].reshape(-1, q.shape[-1])
         out_q[(l, t, h)] = oracle.to_f64(ki.raw_numpy(rows), p["dtype"])
         pos = np.arange(p0, int(geom.seq_lens[s]))
         pg = torch.from_numpy(geom.block_table[s, pos // bs].astype(np.int64)).to(q.device)
@@ -492,7 +492,8 @@ def main():
     log("staged ms: " + ", ".join(f"{s}={avg[s]:.3f}" for s in stages))
 
     # algorithmic work
-    flops = 2.0 * units * G * W * N * p["head_dim"]
+    Wq = ki.scoring_queries(cfg)
+    flops = 2.0 * units * G * Wq * N * p["head_dim"]
     peak = PEAK_BF16_TFLOPS if p["dtype"] == "bf16" else PEAK_F32_TFLOPS
     ach = flops / (avg["score"] * 1e-3) / 1e12
     es = 2 if p["dtype"] == "bf16" else 4

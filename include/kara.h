@@ -8,7 +8,8 @@
  *      |W| window queries over the |W|-|U| compressible window keys, softmax
  *      over keys, column sum over queries.  With grouped-query attention the
  *      G = n_q_heads / n_kv_heads query heads sharing a KV head are all
- *      queries of that head (G*|W| query rows per unit);
+ *      queries of that head (G*|W| query rows per unit).  The query set can
+ *      be narrowed to the window's trailing positions (score_queries);
  *   2. discrete top-k, Eq. (5): budget - alpha positions;
  *   3. Token2Chunk, Eq. (6)-(8), then the fill rule of App. C.3: exactly
  *      `budget` kept positions per unit;
@@ -33,7 +34,9 @@
  *   - Ordering: every ranking is by (value descending, index ascending).
  *
  * Layouts (row-major, contiguous)
- *   q            [n_layers][n_trig][window][n_q_heads][head_dim]   bf16|f32
+ *   q            [n_layers][n_trig][Wq][n_q_heads][head_dim]   bf16|f32,
+ *                the queries of the last Wq window positions (Wq = window
+ *                unless kara_params_t.score_queries says otherwise);
  *                query head hq = kv_head * G + g belongs to KV head kv_head.
  *   pools        per layer [num_pages][n_kv_heads][block_size][head_dim]
  *   block_table  [n_seqs][max_blocks_per_seq] int32, -1 = no page
@@ -63,7 +66,7 @@
 extern "C" {
 #endif
 
-#define KARA_ABI_VERSION 1
+#define KARA_ABI_VERSION 2
 
 /* Largest compressible region |W|-|U| one call supports. */
 #define KARA_MAX_COMPRESSIBLE 4096
@@ -103,6 +106,16 @@ typedef enum kara_status {
  *   max_blocks_per_seq, n_seqs   block-table shape
  *   dtype           KARA_BF16 or KARA_F32 (q and the pools)
  *   scale           logit scale; <= 0 means 1/sqrt(head_dim) (Eq. (1))
+ *   score_queries   Wq, the number of window queries that score the
+ *                   compressible keys -- those of the last Wq window
+ *                   positions -- with the same softmax over the compressible
+ *                   keys and column sum as Eq. (4).  0 or window: every
+ *                   window query (Kara's bidirectional scoring).  buffer: the
+ *                   buffer's queries only (the ablation without bidirectional
+ *                   attention, Sec. 5.3).  With the window spanning the whole
+ *                   cache and chunk_budget 0, the whole-cache top-k of
+ *                   Eq. (2)-(3) scored by a trailing observation window.
+ *                   1 <= Wq <= window otherwise.
  */
 typedef struct kara_params {
   int32_t window;
@@ -119,6 +132,7 @@ typedef struct kara_params {
   int32_t n_seqs;
   int32_t dtype;
   float scale;
+  int32_t score_queries;
 } kara_params_t;
 
 /* Human-readable name of a kara_status_t value.  Never NULL. */

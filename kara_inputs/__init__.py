@@ -25,6 +25,16 @@ Workloads (name -> what it is):
                 sequence's uncompressed fill drawn from 0..W+127, so only the
                 sequences with a full window trigger; pool ~90 % occupied,
                 pages handed out from a shuffled free list.
+* ``buffer_only``  the ``qwen14b`` batch with a 64-token buffer whose queries
+                alone score the compressible 1984 keys (the ablation without
+                bidirectional attention, Sec. 5.3); budget ceil(0.2*1984).
+* ``threshold_topk`` the whole-cache top-k of Eq. (2)-(3) as a baseline:
+                128 sequences, R1-Llama-8B shape (32 layers, 32/8 heads),
+                cache at the threshold C_max = 1280 tokens compressed to
+                1025 (the vLLM+SnapKV setting of App. B.1): the window is the
+                whole cache, its last 32 tokens (observation queries) are
+                kept and score the other 1248, 993 of which are kept by
+                plain top-k (no chunks).
 * ``soak``      128 sequences, 40 layers, 40/8 heads; a 1K prompt, then 31
                 intervals of W=1024 generated tokens (appended 128 at a time,
                 one decode step per append) each ending in a compression
@@ -60,6 +70,14 @@ BASE = {
                    window=1024, buffer=0, budget=205, max_chunk_len=8, chunk_budget=16,
                    block_size=16, num_pages=None, seed=3, prefix=(0, 4096), tail=None,
                    pool_slack="occupancy90", key_mode="normal", fill_max=1024 + 127),
+    "buffer_only": dict(n_seqs=64, n_layers=40, n_q_heads=40, n_kv_heads=8, head_dim=128, dtype="bf16",
+                        window=2048, buffer=64, budget=397, max_chunk_len=8, chunk_budget=16,
+                        block_size=16, num_pages=None, seed=5, prefix=(4096, 16384), tail=(0, 15),
+                        pool_slack=0.10, key_mode="lowrank", score_queries=64),
+    "threshold_topk": dict(n_seqs=128, n_layers=32, n_q_heads=32, n_kv_heads=8, head_dim=128, dtype="bf16",
+                           window=1280, buffer=32, budget=993, max_chunk_len=8, chunk_budget=0,
+                           block_size=16, num_pages=None, seed=6, prefix=(0, 0), tail=(0, 0),
+                           pool_slack=0.10, key_mode="normal", score_queries=32),
     "soak": dict(n_seqs=128, n_layers=40, n_q_heads=40, n_kv_heads=8, head_dim=128, dtype="bf16",
                  window=1024, buffer=0, budget=205, max_chunk_len=8, chunk_budget=16,
                  block_size=16, num_pages=None, seed=4, prefix=(1024, 1024), tail=(0, 0),
@@ -95,7 +113,7 @@ class Geometry:
                     head_dim=c["head_dim"], n_q_heads=c["n_q_heads"], n_kv_heads=c["n_kv_heads"],
                     block_size=c["block_size"], num_pages=self.num_pages,
                     max_blocks_per_seq=self.max_blocks, dtype=c["dtype"], scale=0.0,
-                    n_layers=c["n_layers"])
+                    n_layers=c["n_layers"], score_queries=c.get("score_queries", 0))
 
 
 def _blocks(n_tokens: int, bs: int) -> int:
@@ -183,12 +201,18 @@ def _gen(device, seed):
     return g
 
 
+def scoring_queries(cfg: dict) -> int:
+    """Number of window positions whose queries score (the last ones)."""
+    return cfg.get("score_queries", 0) or cfg["window"]
+
+
 def make_queries(geom: Geometry, layer: int, device="cpu"):
-    """Window queries of one layer: [n_trig, W, Hq, d] ~ N(0,1)."""
+    """Scoring queries of one layer: [n_trig, Wq, Hq, d] ~ N(0,1), Wq the
+    scoring positions (the whole window unless the workload narrows it)."""
     import torch
     c = geom.cfg
     g = _gen(device, c["seed"] * 1_000_003 + 7919 * layer + 1)
-    shape = (len(geom.trig), c["window"], c["n_q_heads"], c["head_dim"])
+    shape = (len(geom.trig), scoring_queries(c), c["n_q_heads"], c["head_dim"])
     return torch.randn(shape, generator=g, device=device, dtype=torch.float32).to(torch_dtype(c))
 
 

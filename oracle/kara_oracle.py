@@ -240,8 +240,19 @@ def validate(p: dict, trig: np.ndarray, block_table: np.ndarray, seq_lens: np.nd
     return status
 
 
+def scoring_queries(p: dict) -> int:
+    """Wq: the window positions whose queries score (the last Wq).  Every
+    position for Kara's Eq. (4); the buffer's alone for the ablation without
+    bidirectional attention (Sec. 5.3), read here as the same softmax over
+    the compressible keys and column sum, over fewer query rows."""
+    return int(p.get("score_queries", 0) or p["window"])
+
+
 def unit_queries(q_raw: np.ndarray, p: dict, layer: int, t: int, head: int) -> np.ndarray:
-    """All query rows scoring KV head `head` (R-GQA): [W*G, d] in fp64."""
+    """All query rows scoring KV head `head` (R-GQA): [Wq*G, d] in fp64.
+    q_raw holds the Wq scoring positions' queries."""
+    if q_raw.shape[2] != scoring_queries(p):
+        raise ValueError(f"q has {q_raw.shape[2]} positions, the parameters score with {scoring_queries(p)}")
     G = p["n_q_heads"] // p["n_kv_heads"]
     rows = q_raw[layer, t, :, head * G:(head + 1) * G, :]     # [W, G, d]
     return to_f64(rows.reshape(-1, rows.shape[-1]), p["dtype"])

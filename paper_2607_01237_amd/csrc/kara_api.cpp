@@ -29,6 +29,7 @@ kara_status_t make_geom(const kara_params_t* p, int32_t n_trig, Geom* g) {
   if ((int64_t)p->max_blocks_per_seq * p->block_size > INT32_MAX) return KARA_ERR_INVALID_ARG;
   if ((int64_t)p->n_q_heads / p->n_kv_heads * W > INT32_MAX / 2) return KARA_ERR_INVALID_ARG;
   if (p->dtype != KARA_BF16 && p->dtype != KARA_F32) return KARA_ERR_INVALID_ARG;
+  if (p->score_queries < 0 || p->score_queries > W) return KARA_ERR_INVALID_ARG;
   if (std::isinf(p->scale)) return KARA_ERR_INVALID_ARG;
   if (p->head_dim != 64 && p->head_dim != 128) return KARA_ERR_UNSUPPORTED;
   // the scoring kernel addresses key rows by 32-bit offsets in 16-byte units
@@ -38,6 +39,7 @@ kara_status_t make_geom(const kara_params_t* p, int32_t n_trig, Geom* g) {
   g->W = W;
   g->U = U;
   g->N = N;
+  g->Wq = p->score_queries > 0 ? p->score_queries : W;
   g->budget = p->budget;
   g->alpha = p->chunk_budget;
   g->gamma = p->max_chunk_len;
@@ -125,7 +127,7 @@ hipError_t run_score(const Geom& g, const ScorePlan& sp, int n_layers, const voi
                      const void* const* k_pools, const int32_t* trig, const int32_t* bt,
                      const int32_t* win_start, const int32_t* status, float* partials,
                      float* scores, hipStream_t stream) {
-  const int64_t q_layer = (int64_t)g.n_trig * g.W * g.Hq * g.d * g.esize;
+  const int64_t q_layer = (int64_t)g.n_trig * g.Wq * g.Hq * g.d * g.esize;
   const int64_t units_layer = (int64_t)g.n_trig * g.Hkv;
   return for_layer_chunks(n_layers, k_pools, nullptr, [&](int l0, int cnt, const PoolPtrs& kp, const PoolPtrs&) {
     return launch_score(g, sp, cnt, (const char*)q + l0 * q_layer, kp, trig, bt, win_start, status,

@@ -15,6 +15,7 @@ constexpr int kMaxLayersPerLaunch = 64;
 // Geometry as the kernels see it (derived once on the host).
 struct Geom {
   int W, U, N;          // window, buffer, compressible length N = W - U
+  int Wq;               // scoring queries per unit (the window's last Wq positions)
   int budget, alpha, gamma;
   int k_disc;           // budget - alpha, Eq. (5)
   int n_chunks;         // floor(alpha / (gamma - 2)), Eq. (7)

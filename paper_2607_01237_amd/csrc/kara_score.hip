@@ -229,12 +229,13 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
   const int s = a.trig[t];
   const int p0 = a.win_start[s];
   const char* kpool = (const char*)a.k.p[l];
-  const char* qunit = a.q + ((int64_t)l * g.n_trig + t) * g.W * g.Hq * (int64_t)C::kRowBytes;
-  const int R = g.G * g.W;
+  const char* qunit = a.q + ((int64_t)l * g.n_trig + t) * g.Wq * g.Hq * (int64_t)C::kRowBytes;
+  const int R = g.G * g.Wq;
   const float c = g.scale * kLog2e;
 
   // ---- this wave's query rows, straight into operand registers ----
-  // row r = w*G + gi (window token w, query head h*G + gi); rows past R
+  // row r = w*G + gi (scoring position w of the Wq in q, query head
+  // h*G + gi); rows past R
   // repeat row 0 and are given no weight
   const int row_base = split * C::kRowsWG + wave * 16 * RT;
   Op qa[RT];
@@ -578,7 +579,7 @@ ScorePlan plan_score(const Geom& g, int64_t n_units) {
   (void)n_units;
   ScorePlan sp{};
   sp.rows_wg = kScoreWaves * 16 * row_tiles(g);
-  const int64_t rows = (int64_t)g.G * g.W;
+  const int64_t rows = (int64_t)g.G * g.Wq;
   sp.n_splits = (int)((rows + sp.rows_wg - 1) / sp.rows_wg);
   return sp;
 }

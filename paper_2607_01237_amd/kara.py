@@ -44,6 +44,7 @@ class KaraParams(ctypes.Structure):
         ("n_seqs", ctypes.c_int32),
         ("dtype", ctypes.c_int32),
         ("scale", ctypes.c_float),
+        ("score_queries", ctypes.c_int32),
     ]
 
 
@@ -53,7 +54,8 @@ def make_params(p: dict, n_seqs: int) -> KaraParams:
     dt = BF16 if dt in ("bf16", BF16) else F32 if dt in ("f32", F32) else dt
     return KaraParams(p["window"], p["buffer"], p["budget"], p["chunk_budget"], p["max_chunk_len"],
                       p["head_dim"], p["n_q_heads"], p["n_kv_heads"], p["block_size"], p["num_pages"],
-                      p["max_blocks_per_seq"], n_seqs, dt, float(p.get("scale", 0.0) or 0.0))
+                      p["max_blocks_per_seq"], n_seqs, dt, float(p.get("scale", 0.0) or 0.0),
+                      int(p.get("score_queries", 0) or 0))
 
 
 _VP = ctypes.c_void_p

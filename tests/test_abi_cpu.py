@@ -35,7 +35,7 @@ def test_exports_every_declared_function(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert kara.abi_version() == 1
+    assert kara.abi_version() == 2
     for code in (0, -1, -2, -3, -4):
         assert kara.status_string(code).startswith("KARA_")
     assert "unknown" in kara.status_string(12345)
@@ -66,6 +66,8 @@ def test_workspace_size_scales(lib):
     ("dtype", 7, kara.ERR_INVALID_ARG),
     ("block_size", 0, kara.ERR_INVALID_ARG),
     ("scale", float("inf"), kara.ERR_INVALID_ARG),
+    ("score_queries", -1, kara.ERR_INVALID_ARG),
+    ("score_queries", 1025, kara.ERR_INVALID_ARG),
 ])
 def test_bad_params_rejected(lib, field, value, code):
     p = good_params()
@@ -126,3 +128,11 @@ def test_harness_checks_before_launch(lib):
     wide = good_params(n_q_heads=256, n_kv_heads=8)
     assert lib.kara_harness_decode_attention(ctypes.byref(wide), 4, fake, 1, fake, pools, pools, fake, fake, 1000,
                                              fake, fake, 1 << 30, None) == kara.ERR_UNSUPPORTED
+
+
+def test_scoring_queries_shrink_the_workspace(lib):
+    # the partial column sums scale with the scoring rows (G * Wq)
+    full = kara.workspace_size(good_params(), 8, 1)
+    part = kara.workspace_size(good_params(buffer=64, budget=192, score_queries=64), 8, 1)
+    assert part < full
+    assert kara.workspace_size(good_params(score_queries=1024), 8, 1) == full

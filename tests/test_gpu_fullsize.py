@@ -58,7 +58,7 @@ def test_fullsize_sampled(name, n_p1, n_p2):
     print(f"\n[case] {name} full size: {L} layers x {nt} triggered x {H} heads, W={W}", flush=True)
 
     dt = ki.torch_dtype(cfg)
-    q = torch.empty((L, nt, W, p["n_q_heads"], p["head_dim"]), dtype=dt, device=dev)
+    q = torch.empty((L, nt, ki.scoring_queries(cfg), p["n_q_heads"], p["head_dim"]), dtype=dt, device=dev)
     kp, vp = [], []
     for l in range(L):
         q[l] = ki.make_queries(geom, l, dev)

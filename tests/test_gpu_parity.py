@@ -131,3 +131,16 @@ def test_outlier_keys(pos, scale):
         # product with it is positive, about half of the G*W rows
         w = gpu["scores"][0, :, :, pos]
         assert (w > 0.25 * case.p["n_q_heads"] // case.p["n_kv_heads"] * case.p["window"]).all()
+
+
+def test_buffer_only_scoring():
+    # the ablation without bidirectional attention: only the 64 buffer
+    # queries score the 960 compressible keys (q holds those 64 positions)
+    _run(ki.workload("buffer_only", n_seqs=3, n_layers=2, window=1024, budget=192, prefix=(0, 300)))
+
+
+def test_threshold_topk_baseline():
+    # Eq. (2)-(3): the whole cache (1280 tokens at the threshold) is the
+    # window, its last 32 tokens score and are kept, plain top-k of 993
+    case, rep, gpu = _run(ki.workload("threshold_topk", n_seqs=3, n_layers=2))
+    assert (gpu["seq_lens"][case.geom.trig] == 1025).all()

@@ -134,3 +134,38 @@ def test_round_scores_is_nearest_even():
     x = np.array([1.0 + 2.0 ** -24, 1.0 + 3 * 2.0 ** -24])
     r = oracle.round_scores(x)
     assert r[0] == np.float32(1.0) and r[1] == np.float32(1.0 + 2.0 ** -22)
+
+
+def test_scoring_queries_split_rows_additively():
+    # Column sums of per-row softmaxes add over disjoint query sets: scoring
+    # with the first W-U positions' queries plus scoring with the last U
+    # (the buffer alone, the ablation without bidirectional attention of
+    # Sec. 5.3) gives Kara's score with all W.  A slip that took the wrong
+    # rows for the narrowed set, or normalised over the query subset, breaks
+    # the identity; each part also sums to its own number of rows.
+    G, Hkv, W, U, d = 2, 2, 10, 3, 8
+    q, pool, table, bs = _pool_case(G, Hkv, W, d, "f32", 5)
+    p = dict(window=W, buffer=U, block_size=bs, n_q_heads=G * Hkv, n_kv_heads=Hkv,
+             head_dim=d, dtype="f32", scale=0.0)
+    p0 = 1
+    full = oracle.score_units(p, [0], q, [pool], table, np.array([p0]), [(0, 0, 1)])[0]
+    tail = oracle.score_units(dict(p, score_queries=U), [0], np.ascontiguousarray(q[:, :, W - U:]), [pool],
+                              table, np.array([p0]), [(0, 0, 1)])[0]
+    keys = oracle.unit_keys(pool, p, table[0], p0, 1)
+    front = sum(oracle.window_scores(q[0, 0, :W - U, h, :].astype(np.float64), keys, 1 / math.sqrt(d))
+                for h in (2, 3))
+    np.testing.assert_allclose(front + tail, full, rtol=1e-12)
+    assert abs(tail.sum() - G * U) < 1e-12
+    # the buffer rows are the ones scoring: position W-1's query head 3
+    # alone, as a single softmax row, is one term of the tail score
+    last = oracle.window_scores(q[0, 0, W - 1:, 3, :].astype(np.float64), keys, 1 / math.sqrt(d))
+    assert (tail >= last - 1e-15).all()
+
+
+def test_scoring_queries_shape_checked():
+    G, Hkv, W, d = 1, 1, 6, 8
+    q, pool, table, bs = _pool_case(G, Hkv, W, d, "f32", 2)
+    p = dict(window=W, buffer=2, block_size=bs, n_q_heads=1, n_kv_heads=1, head_dim=d, dtype="f32",
+             scale=0.0, score_queries=2)
+    with pytest.raises(ValueError):
+        oracle.unit_queries(q, p, 0, 0, 0)
