@@ -562,14 +562,41 @@ __global__ __launch_bounds__(256) void split_sum_kernel(const float* __restrict_
   scores[u * (int64_t)N + j] = v;
 }
 
-// row tiles per wave: four (512 rows per workgroup); two for fp32 with
-// 128-wide heads, whose operands take twice the registers
-int row_tiles(const Geom& g) { return (g.dtype == KARA_F32 && g.d == 128) ? 2 : 4; }
+// Row tiles per wave.  At most four (512 rows per workgroup), two for fp32
+// with 128-wide heads, whose operands take twice the registers.  Fewer when
+// a unit has few query rows (scoring by a buffer or an observation window):
+// the count that pads the unit's rows least, the larger one on a tie, since
+// each workgroup streams all of the unit's keys.
+int row_tiles(const Geom& g) {
+  const int max_rt = (g.dtype == KARA_F32 && g.d == 128) ? 2 : 4;
+  const int64_t rows = (int64_t)g.G * g.Wq;
+  int best = max_rt;
+  int64_t best_pad = -1;
+  for (int rt = max_rt; rt >= 1; --rt) {
+    const int64_t per = (int64_t)kScoreWaves * 16 * rt;
+    const int64_t pad = (rows + per - 1) / per * per - rows;
+    if (best_pad < 0 || pad < best_pad) {
+      best = rt;
+      best_pad = pad;
+    }
+  }
+  return best;
+}
 
 template <int DT, int D>
-hipError_t launch_d(const ScoreArgs& a, hipStream_t stream) {
-  constexpr int RT = (DT == KARA_F32 && D == 128) ? 2 : 4;
-  hipLaunchKernelGGL((score_kernel<DT, D, RT>), dim3((unsigned)a.n_blocks), dim3(kScoreThreads), 0, stream, a);
+hipError_t launch_d(const ScoreArgs& a, int rt, hipStream_t stream) {
+  const dim3 grid((unsigned)a.n_blocks), block(kScoreThreads);
+  if constexpr (DT == KARA_F32 && D == 128) {
+    if (rt == 1) hipLaunchKernelGGL((score_kernel<DT, D, 1>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((score_kernel<DT, D, 2>), grid, block, 0, stream, a);
+  } else {
+    switch (rt) {
+      case 1: hipLaunchKernelGGL((score_kernel<DT, D, 1>), grid, block, 0, stream, a); break;
+      case 2: hipLaunchKernelGGL((score_kernel<DT, D, 2>), grid, block, 0, stream, a); break;
+      case 3: hipLaunchKernelGGL((score_kernel<DT, D, 3>), grid, block, 0, stream, a); break;
+      default: hipLaunchKernelGGL((score_kernel<DT, D, 4>), grid, block, 0, stream, a); break;
+    }
+  }
   return hipGetLastError();
 }
 
@@ -601,9 +628,12 @@ hipError_t launch_score(const Geom& g, const ScorePlan& sp, int n_layers, const 
   a.n_splits = sp.n_splits;
   a.n_blocks = (int64_t)n_layers * g.n_trig * g.Hkv * sp.n_splits;
   if (a.n_blocks == 0) return hipSuccess;
+  const int rt = sp.rows_wg / (kScoreWaves * 16);
   hipError_t e;
-  if (g.dtype == KARA_BF16) e = g.d == 128 ? launch_d<KARA_BF16, 128>(a, stream) : launch_d<KARA_BF16, 64>(a, stream);
-  else e = g.d == 128 ? launch_d<KARA_F32, 128>(a, stream) : launch_d<KARA_F32, 64>(a, stream);
+  if (g.dtype == KARA_BF16)
+    e = g.d == 128 ? launch_d<KARA_BF16, 128>(a, rt, stream) : launch_d<KARA_BF16, 64>(a, rt, stream);
+  else
+    e = g.d == 128 ? launch_d<KARA_F32, 128>(a, rt, stream) : launch_d<KARA_F32, 64>(a, rt, stream);
   if (e != hipSuccess || sp.n_splits == 1) return e;
   const int64_t units = a.n_blocks / sp.n_splits;
   hipLaunchKernelGGL(split_sum_kernel, dim3((unsigned)units, (unsigned)((g.N + 255) / 256)), dim3(256), 0, stream,
