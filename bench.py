@@ -10,13 +10,13 @@ keep whatever the previous step left, so every step compresses a full
 window of the same shape.
 
 Prints one JSON line.  `value` is window tokens compressed per second
-(triggered sequences x window length per step / step time).  `roofline`
+(triggered sequences x windows x window length per step / step time).  `roofline`
 covers the dominant kernel (scoring) from a staged pass that times each
 stage with HIP events on the launch stream; `roofline_select_compact` covers
 the HBM-bound stages.  `cpu_baseline` times the CPU oracle on a bounded
 sample of units on this host.
 
-    python bench.py [--steps K] [--warmup W] [--workload qwen14b|batch8|ragged|tiny]
+    python bench.py [--steps K] [--warmup W] [--workload qwen14b|batch8|ragged|buffer_only|threshold_topk|prefill]
     python bench.py --workload soak [--intervals n] [--warmup W]
 
 The soak runs the compression step inside a decode loop (append, decode
@@ -185,7 +185,9 @@ def setup(cfg, device):
     p = geom.params()
     L, nt = cfg["n_layers"], len(geom.trig)
     dt = ki.torch_dtype(cfg)
-    q = torch.empty((L, nt, ki.scoring_queries(cfg), cfg["n_q_heads"], cfg["head_dim"]), dtype=dt, device=device)
+    nw = cfg.get("n_windows", 1)
+    q = torch.empty((L, nt) + ((nw,) if nw > 1 else ()) + (ki.scoring_queries(cfg), cfg["n_q_heads"],
+                                                            cfg["head_dim"]), dtype=dt, device=device)
     kp, vp = [], []
     for l in range(L):
         q[l] = ki.make_queries(geom, l, device)
@@ -204,22 +206,29 @@ def setup(cfg, device):
 
 
 def moved_rows(kept, p, tails):
-    """Rows that change place in one step (kept rows not already in place plus
-    the buffer and tail rows that shift down), per unit."""
+    """Rows that change place in one step, per (layer, trigger, head): kept
+    rows not already at their destination plus the rows after the last
+    window's compressible region (its buffer and the tail), which shift down.
+    kept: [L, nt, n_windows, H, budget]; tails: rows after the last window."""
     budget, W, U = p["budget"], p["window"], p["buffer"]
+    N = W - U
+    nw = kept.shape[2]
+    w = np.arange(nw)[:, None]
     j = np.arange(budget)
-    in_place = (kept == j).sum(axis=-1)                     # [L, nt, H]
-    shift = (W - U) - budget                                # positions the buffer/tail move by
+    in_place = (kept.transpose(0, 1, 3, 2, 4) + w * N == w * budget + j).sum(axis=(-2, -1))   # [L, nt, H]
+    shift = nw * (N - budget)                                # positions the buffer/tail move by
     extra = (U + tails[None, :, None]) * (1 if shift > 0 else 0)
-    return (budget - in_place) + extra
+    return (nw * budget - in_place) + extra
 
 
-def cpu_baseline(geom, p, q, kp, vp, budget_s):
+def cpu_baseline(geom, p, q, kp, vp, budget_s, n_windows=1):
     """The oracle, as it stands, on whole units of the workload.
 
-    Units of layer 0 (sequence by sequence, every KV head) are copied to the
-    host in batches and run through the oracle's scoring, selection,
-    Token2Chunk, fill and K/V gather until `budget_s` seconds have passed.
+    Units of layer 0 (sequence by sequence, window by window, every KV head)
+    are copied to the host in batches and run through the oracle's scoring,
+    selection, Token2Chunk, fill and K/V gather until `budget_s` seconds have
+    passed.  With one window a unit's rows are its window and the tail after
+    it; with several, the unit's own window.
     """
     from concurrent.futures import ThreadPoolExecutor
 
@@ -231,7 +240,7 @@ def cpu_baseline(geom, p, q, kp, vp, budget_s):
     scale = oracle.scale_of(p)
 
     def one(args):
-        qa, ka, va = args                      # ka, va: window + tail rows
+        qa, ka, va = args
         a = oracle.round_scores(oracle.window_scores(qa, ka[:N], scale))
         _, kept = oracle.kept_set(a, p["budget"], p["chunk_budget"], p["max_chunk_len"])
         oracle.gather_rows(ka, kept, W, U)
@@ -239,12 +248,12 @@ def cpu_baseline(geom, p, q, kp, vp, budget_s):
         return 1
 
     H = p["n_kv_heads"]
-    all_units = [(0, t, h) for t in range(len(geom.trig)) for h in range(H)]
+    all_units = [(0, t, w, h) for t in range(len(geom.trig)) for w in range(n_windows) for h in range(H)]
     done, busy = 0, 0.0
     with ThreadPoolExecutor(threads) as ex:
         for i in range(0, len(all_units), threads):
             batch = all_units[i:i + threads]
-            hq, hk, hv = host_units(geom, p, q, kp, vp, batch)
+            hq, hk, hv = host_units(geom, p, q, kp, vp, batch, n_windows)
             t0 = time.perf_counter()
             done += sum(ex.map(one, [(hq[u], hk[u], hv[u]) for u in batch]))
             busy += time.perf_counter() - t0
@@ -253,26 +262,28 @@ def cpu_baseline(geom, p, q, kp, vp, budget_s):
     return done, busy, threads
 
 
-def host_units(geom, p, q, kp, vp, units):
-    """Host fp64 copies of the listed units' queries and window+tail K/V rows."""
+def host_units(geom, p, q, kp, vp, units, n_windows=1):
+    """Host fp64 copies of the listed (layer, trigger, window, head) units'
+    queries and K/V rows (window and tail with one window, else the window)."""
     import torch
 
     import kara_inputs as ki
     import oracle
 
     H, G, W = p["n_kv_heads"], p["n_q_heads"] // p["n_kv_heads"], p["window"]
-    bs = p["block_size"]
+    N, bs = W - p["buffer"], p["block_size"]
     out_q, out_k, out_v = {}, {}, {}
-    for (l, t, h) in units:
+    for (l, t, w, h) in units:
         s = int(geom.trig[t])
-        p0 = int(geom.win_start[s])
-        rows = q[l, t, :, h * G:(h + 1) * G, :].reshape(-1, q.shape[-1])
-        out_q[(l, t, h)] = oracle.to_f64(ki.raw_numpy(rows), p["dtype"])
-        pos = np.arange(p0, int(geom.seq_lens[s]))
+        p0 = int(geom.win_start[s]) + w * N
+        qw = q[l, t] if n_windows == 1 else q[l, t, w]
+        rows = qw[:, h * G:(h + 1) * G, :].reshape(-1, q.shape[-1])
+        out_q[(l, t, w, h)] = oracle.to_f64(ki.raw_numpy(rows), p["dtype"])
+        pos = np.arange(p0, int(geom.seq_lens[s]) if n_windows == 1 else p0 + W)
         pg = torch.from_numpy(geom.block_table[s, pos // bs].astype(np.int64)).to(q.device)
         sl = torch.from_numpy((pos % bs).astype(np.int64)).to(q.device)
-        out_k[(l, t, h)] = oracle.to_f64(ki.raw_numpy(kp[l][pg, h, sl, :]), p["dtype"])
-        out_v[(l, t, h)] = oracle.to_f64(ki.raw_numpy(vp[l][pg, h, sl, :]), p["dtype"])
+        out_k[(l, t, w, h)] = oracle.to_f64(ki.raw_numpy(kp[l][pg, h, sl, :]), p["dtype"])
+        out_v[(l, t, w, h)] = oracle.to_f64(ki.raw_numpy(vp[l][pg, h, sl, :]), p["dtype"])
     return out_q, out_k, out_v
 
 
@@ -411,27 +422,57 @@ def main():
     L, nt, H = cfg["n_layers"], len(geom.trig), p["n_kv_heads"]
     W, U, N = p["window"], p["buffer"], p["window"] - p["buffer"]
     G = p["n_q_heads"] // H
+    nw = cfg.get("n_windows", 1)
     units = L * nt * H
     log(f"setup {time.perf_counter() - t_setup:.1f}s: {args.workload} units={units} pages={geom.num_pages} "
         f"mem={torch.cuda.memory_allocated() / 2**30:.1f} GiB")
 
     stream = torch.cuda.current_stream()
-    ws = torch.empty(kara.workspace_size(params, nt, L), dtype=torch.uint8, device=device)
+    ws_bytes = kara.workspace_size(params, nt * nw, L)
     status = torch.empty(nt, dtype=torch.int32, device=device)
     freed = torch.empty((nt, p["max_blocks_per_seq"]), dtype=torch.int32, device=device)
     n_freed = torch.empty(nt, dtype=torch.int32, device=device)
-    scores = torch.empty((L, nt, H, N), dtype=torch.float32, device=device)
-    disc = torch.empty((L, nt, H, p["budget"] - p["chunk_budget"]), dtype=torch.int32, device=device)
-    kept = torch.empty((L, nt, H, p["budget"]), dtype=torch.int32, device=device)
+    # [L, trigger, window, head, ...]: with one window the same memory as [L, trigger, head, ...]
+    scores = torch.empty((L, nt * nw, H, N), dtype=torch.float32, device=device)
+    disc = torch.empty((L, nt * nw, H, p["budget"] - p["chunk_budget"]), dtype=torch.int32, device=device)
+    kept = torch.empty((L, nt * nw, H, p["budget"]), dtype=torch.int32, device=device)
 
     def restore():
         meta["bt"].copy_(meta["bt0"], non_blocking=True)
         meta["seq_lens"].copy_(meta["seq_lens0"], non_blocking=True)
 
+    def compress():
+        if nw == 1:
+            kara.compress_window(params, meta["trig"], q, kp, vp, meta["bt"], meta["seq_lens"], meta["win_start"],
+                                 True, status, ws, kept=kept, freed=freed, n_freed=n_freed, stream=stream)
+        else:
+            kara.compress_prefill(params, meta["trig"], nw, q, kp, vp, meta["bt"], meta["seq_lens"],
+                                  meta["win_start"], True, status, ws, kept=kept, freed=freed, n_freed=n_freed,
+                                  stream=stream)
+
     def step():
         restore()
-        kara.compress_window(params, meta["trig"], q, kp, vp, meta["bt"], meta["seq_lens"], meta["win_start"], True,
-                             status, ws, kept=kept, freed=freed, n_freed=n_freed, stream=stream)
+        compress()
+
+    # The staged pass times scoring and selection through the single-window
+    # entry points.  Prefill's windows are scored as separate sequences then:
+    # window w of sequence s becomes a sequence of its own that shares s's
+    # block-table row and length and starts its window w*(W-U) later, so the
+    # scoring launch covers the same (layer, trigger, window, head) units in
+    # the same order over the same queries.
+    if nw == 1:
+        sv = dict(params=params, trig=meta["trig"], bt=meta["bt"], seq_lens=meta["seq_lens"],
+                  win_start=meta["win_start"], status=status)
+    else:
+        tr = geom.trig.astype(np.int64)
+        rep = lambda a: torch.from_numpy(np.ascontiguousarray(np.repeat(a, nw, axis=0))).to(device)
+        ws_v = np.repeat(geom.win_start[tr], nw) + np.tile(np.arange(nw, dtype=np.int32) * N, nt)
+        sv = dict(params=kara.make_params(p, nt * nw), trig=torch.arange(nt * nw, dtype=torch.int32, device=device),
+                  bt=rep(geom.block_table[tr]), seq_lens=rep(geom.seq_lens[tr]),
+                  win_start=torch.from_numpy(ws_v.astype(np.int32)).to(device),
+                  status=torch.empty(nt * nw, dtype=torch.int32, device=device))
+    q_v = q.view((L, nt * nw) + tuple(q.shape[-3:]))
+    ws = torch.empty(max(ws_bytes, kara.workspace_size(sv["params"], nt * nw, L)), dtype=torch.uint8, device=device)
 
     if args.copy_calibration_gib > 0:
         n = int(args.copy_calibration_gib * 2**30) // 2
@@ -463,7 +504,10 @@ def main():
         f"{np.median(step_ms):.3f} ms")
 
     # staged pass: the same path through the per-stage entry points, with HIP
-    # events between stages on the launch stream
+    # events between stages on the launch stream.  With several windows the
+    # compaction and commit have no entry points of their own: the whole
+    # prefill call is timed after the staged scoring and selection, and
+    # compact+commit is its time less theirs.
     stages = ["score", "select_t2c", "compact", "commit"]
     times = {s: [] for s in stages}
     n_stage = max(3, args.steps)
@@ -471,17 +515,21 @@ def main():
         restore()
         e = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
         e[0].record(stream)
-        kara.score_window(params, meta["trig"], q, kp, meta["bt"], meta["seq_lens"], meta["win_start"], scores,
-                          status, ws, stream=stream)
+        kara.score_window(sv["params"], sv["trig"], q_v, kp, sv["bt"], sv["seq_lens"], sv["win_start"], scores,
+                          sv["status"], ws, stream=stream)
         e[1].record(stream)
         kara.select(params, scores, disc, stream=stream)
         kara.token2chunk(params, scores, disc, kept, stream=stream)
         e[2].record(stream)
-        kara.compact_pages(params, meta["trig"], kept, kp, vp, meta["bt"], meta["seq_lens"], meta["win_start"],
-                           status, stream=stream)
-        e[3].record(stream)
-        kara.commit_tables(params, meta["trig"], meta["bt"], meta["seq_lens"], meta["win_start"], freed, n_freed,
-                           status, stream=stream)
+        if nw == 1:
+            kara.compact_pages(params, meta["trig"], kept, kp, vp, meta["bt"], meta["seq_lens"], meta["win_start"],
+                               status, stream=stream)
+            e[3].record(stream)
+            kara.commit_tables(params, meta["trig"], meta["bt"], meta["seq_lens"], meta["win_start"], freed,
+                               n_freed, status, stream=stream)
+        else:
+            compress()
+            e[3].record(stream)
         e[4].record(stream)
         torch.cuda.synchronize()
         if i == 0:
@@ -489,24 +537,28 @@ def main():
         for k, s in enumerate(stages):
             times[s].append(e[k].elapsed_time(e[k + 1]))
     avg = {s: float(np.mean(v)) for s, v in times.items()}
+    if nw > 1:
+        avg["compact"] = max(0.0, avg["compact"] - avg["score"] - avg["select_t2c"])
+    st_v = sv["status"].cpu().numpy()
+    assert (st_v == 0).all(), f"unexpected staged status {st_v}"
     log("staged ms: " + ", ".join(f"{s}={avg[s]:.3f}" for s in stages))
 
     # algorithmic work
     Wq = ki.scoring_queries(cfg)
-    flops = 2.0 * units * G * Wq * N * p["head_dim"]
+    flops = 2.0 * units * nw * G * Wq * N * p["head_dim"]
     peak = PEAK_BF16_TFLOPS if p["dtype"] == "bf16" else PEAK_F32_TFLOPS
     ach = flops / (avg["score"] * 1e-3) / 1e12
     es = 2 if p["dtype"] == "bf16" else 4
     row_bytes = p["head_dim"] * es
-    tails = (geom.seq_lens[geom.trig] - geom.win_start[geom.trig] - W).astype(np.int64)
-    mv = moved_rows(kept.cpu().numpy(), p, tails)
+    tails = (geom.seq_lens[geom.trig] - geom.win_start[geom.trig] - (nw - 1) * N - W).astype(np.int64)
+    mv = moved_rows(kept.cpu().numpy().reshape(L, nt, nw, H, p["budget"]), p, tails)
     compact_bytes = float(mv.sum()) * row_bytes * 2 * 2          # read + write, K and V
-    select_bytes = float(units) * (N * 4 + p["budget"] * 4 + (p["budget"] - p["chunk_budget"]) * 4 * 2)
+    select_bytes = float(units * nw) * (N * 4 + p["budget"] * 4 + (p["budget"] - p["chunk_budget"]) * 4 * 2)
     sc_ms = avg["select_t2c"] + avg["compact"]
     sc_gbs = (compact_bytes + select_bytes) / (sc_ms * 1e-3) / 1e9
 
     ms = wall * 1e3 / args.steps
-    win_tokens = nt * W
+    win_tokens = nt * nw * W
     traffic = load_traffic(args.workload)
     result = {
         "metric": "window tokens compressed/s (score+select+compact); % MFMA peak / % HBM GB/s",
@@ -526,7 +578,7 @@ def main():
             "workload": args.workload, "sequences": int(nt), "layers": L, "q_heads": p["n_q_heads"],
             "kv_heads": H, "head_dim": p["head_dim"], "window": W, "buffer": U, "budget": p["budget"],
             "chunk_budget": p["chunk_budget"], "max_chunk_len": p["max_chunk_len"], "block_size": p["block_size"],
-            "pages": int(geom.num_pages), "units_per_step": int(units),
+            "pages": int(geom.num_pages), "units_per_step": int(units * nw), "windows_per_sequence": nw,
         },
         "roofline": {
             "kernel": "score_kernel (window scoring, Eq. 4)",
@@ -542,12 +594,12 @@ def main():
     }
 
     if not args.no_cpu_baseline:
-        done, dt_cpu, threads = cpu_baseline(geom, p, q, kp, vp, args.cpu_seconds)
+        done, dt_cpu, threads = cpu_baseline(geom, p, q, kp, vp, args.cpu_seconds, nw)
         # units per window token: every window token is compressed in L*H units
         rate = done / dt_cpu * W / (L * H)
         result["cpu_baseline"] = {
             "value": rate, "unit": "window tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"{done} whole (sequence, KV head) units of layer 0 of this workload: fp64 scoring, "
+            "sample": f"{done} whole (sequence, window, KV head) units of layer 0 of this workload: fp64 scoring, "
                       f"selection, Token2Chunk, fill and K/V gather in {dt_cpu:.1f} s of oracle time; one window "
                       f"token is compressed in layers*kv_heads units, so rate = units/s * W/(layers*kv_heads)",
         }

@@ -232,6 +232,38 @@ kara_status_t kara_compress_window(const kara_params_t* p, int32_t n_trig, const
                                    int32_t* n_freed, int32_t* status, void* workspace,
                                    size_t workspace_bytes, void* stream);
 
+/*
+ * Prefill-time compression (App. C.2): the prompt's KV pairs compressed
+ * window by window, all windows at once.  Sequence s = trig[t] holds
+ * n_windows consecutive windows starting at win_start[s], window w covering
+ * [win_start + w*(W-U), win_start + w*(W-U) + W): consecutive windows share
+ * the U buffer positions, whose queries score both and whose keys belong to
+ * the next window's compressible region.  Each window is one unit per layer
+ * and KV head, scored by its own queries (Eq. (4)) and selected on its own
+ * (Eq. (5)-(8), App. C.3).  Compaction then leaves, in order, every window's
+ * `budget` kept rows and everything after the last window's compressible
+ * region (its buffer and the rest of the sequence); the commit shortens the
+ * sequence by n_windows * (window - buffer - budget).  One window is
+ * kara_compress_window.  The next decode-time window of a compressed
+ * sequence starts at win_start + n_windows * budget.
+ *
+ * Layouts gain a window index after the trigger:
+ *   q       [n_layers][n_trig][n_windows][Wq][n_q_heads][head_dim]
+ *   scores  [n_layers][n_trig][n_windows][n_kv_heads][window - buffer]
+ *   discrete, kept  [n_layers][n_trig][n_windows][n_kv_heads][...]
+ * The workspace is sized by kara_workspace_size(p, n_trig * n_windows,
+ * n_layers).  A sequence too short for its windows is flagged
+ * KARA_SEQ_BAD_WINDOW.  n_windows < 1, or windows longer than a block-table
+ * row, is KARA_ERR_INVALID_ARG.
+ */
+kara_status_t kara_compress_prefill(const kara_params_t* p, int32_t n_trig, const int32_t* trig,
+                                    int32_t n_windows, int32_t n_layers, const void* q,
+                                    void* const* k_pools, void* const* v_pools, int32_t* block_table,
+                                    int32_t* seq_lens, const int32_t* win_start, int32_t commit,
+                                    float* scores, int32_t* discrete, int32_t* kept, int32_t* freed,
+                                    int32_t* n_freed, int32_t* status, void* workspace,
+                                    size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -35,6 +35,10 @@ Workloads (name -> what it is):
                 whole cache, its last 32 tokens (observation queries) are
                 kept and score the other 1248, 993 of which are kept by
                 plain top-k (no chunks).
+* ``prefill``   16 prompts of 16K-17K tokens, Qwen3-8B shape (36 layers,
+                32/8 heads), compressed before decoding in 16 windows of
+                W=1024 each (App. C.2), budget 205 per window; the prompt's
+                last 0-1023 tokens (short of a window) stay uncompressed.
 * ``soak``      128 sequences, 40 layers, 40/8 heads; a 1K prompt, then 31
                 intervals of W=1024 generated tokens (appended 128 at a time,
                 one decode step per append) each ending in a compression
@@ -78,6 +82,10 @@ BASE = {
                            window=1280, buffer=32, budget=993, max_chunk_len=8, chunk_budget=0,
                            block_size=16, num_pages=None, seed=6, prefix=(0, 0), tail=(0, 0),
                            pool_slack=0.10, key_mode="normal", score_queries=32),
+    "prefill": dict(n_seqs=16, n_layers=36, n_q_heads=32, n_kv_heads=8, head_dim=128, dtype="bf16",
+                    window=1024, buffer=0, budget=205, max_chunk_len=8, chunk_budget=16,
+                    block_size=16, num_pages=None, seed=7, prefix=(0, 0), tail=(0, 1023),
+                    pool_slack=0.10, key_mode="normal", n_windows=16),
     "soak": dict(n_seqs=128, n_layers=40, n_q_heads=40, n_kv_heads=8, head_dim=128, dtype="bf16",
                  window=1024, buffer=0, budget=205, max_chunk_len=8, chunk_budget=16,
                  block_size=16, num_pages=None, seed=4, prefix=(1024, 1024), tail=(0, 0),
@@ -136,7 +144,9 @@ def make_geometry(cfg: dict) -> Geometry:
         tlo, thi = cfg["tail"]
         tail = rng.integers(tlo, thi + 1, B)
         trig = np.arange(B)
-        seq_lens = prefix + W + tail
+        # n_windows consecutive windows (prefill) advance by W - U
+        nw = cfg.get("n_windows", 1)
+        seq_lens = prefix + (nw - 1) * (W - cfg["buffer"]) + W + tail
         win_start = prefix
     need = np.array([_blocks(int(L), bs) for L in seq_lens])
     max_blocks = int(cfg.get("max_blocks") or need.max())
@@ -213,6 +223,8 @@ def make_queries(geom: Geometry, layer: int, device="cpu"):
     c = geom.cfg
     g = _gen(device, c["seed"] * 1_000_003 + 7919 * layer + 1)
     shape = (len(geom.trig), scoring_queries(c), c["n_q_heads"], c["head_dim"])
+    if c.get("n_windows", 1) > 1:       # prefill: [n_trig, n_windows, Wq, Hq, d]
+        shape = (shape[0], c["n_windows"]) + shape[1:]
     return torch.randn(shape, generator=g, device=device, dtype=torch.float32).to(torch_dtype(c))
 
 

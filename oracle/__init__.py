@@ -9,5 +9,5 @@ from .kara_oracle import (  # noqa: F401
     bf16_bits_to_f64, to_f64, window_scores, round_scores, rank_order, discrete_topk,
     chunk_candidates, token2chunk, fill_positions, kept_set, compaction_map, gather_rows,
     released_blocks, read_rows, write_rows, validate, scoring_queries, unit_queries, unit_keys, scale_of,
-    score_units, compress,
+    score_units, compress, compress_prefill,
 )

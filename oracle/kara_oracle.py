@@ -33,6 +33,13 @@ the place it is used):
   original order, then the buffer, then the tokens after the window.
 * R-PAGES: compaction is in place in the window's own pages; the trailing
   logical blocks no longer needed are released in ascending order.
+* R-PREFILL: prompt windows advance by |W|-|U| like decode-time windows, so
+  consecutive windows share the |U| buffer positions (queries of both,
+  compressible keys of the later one); all windows are scored and selected
+  independently and at once.
+* R-QSUBSET: scoring with part of the window's queries (the ablation that
+  uses the buffer's queries only, Sec. 5.3) keeps Eq. (4)'s softmax over the
+  compressible keys and column sum, over fewer rows.
 """
 
 from __future__ import annotations
@@ -336,6 +343,80 @@ def compress(p: dict, trig, q_raw, k_pools, v_pools, block_table, seq_lens, win_
                     write_rows(pool, block_table[s], pos[:after.shape[0]], h, bs, after)
         if commit:
             new_len = sl - (N - budget)
+            blocks = released_blocks(sl, new_len, bs)
+            freed.append([int(block_table[s, b]) for b in blocks])
+            n_freed[t] = len(blocks)
+            block_table[s, blocks] = -1
+            seq_lens[s] = new_len
+        else:
+            freed.append([])
+    return dict(status=status, scores=scores, discrete=disc, kept=kept, freed=freed, n_freed=n_freed)
+
+
+def compress_prefill(p: dict, trig, n_windows: int, q_raw, k_pools, v_pools, block_table, seq_lens,
+                     win_start, commit: bool = True, threads: int = 0, score_override=None):
+    """Prefill-time compression (App. C.2) on host copies (mutated in place).
+
+    The prompt of sequence s = trig[t] is split into n_windows windows,
+    window w covering [p0 + w*(W-U), p0 + w*(W-U) + W) with p0 = win_start[s]
+    (the window advances by W-U, as it does during decoding).  Each window is
+    scored by its own queries q_raw[l, t, w] (Eq. (4)) and selected on its
+    own (Eq. (5)-(8), App. C.3), all windows at once.  The cache then holds,
+    in order, each window's kept rows and everything after the last window's
+    compressible region (R-ORDER applied window by window), and the sequence
+    is n_windows * (W-U-budget) shorter.
+
+    q_raw: [L, n_trig, n_windows, Wq, Hq, d]; scores, discrete and kept gain
+    the window axis after the trigger.
+    """
+    trig = np.asarray(trig, dtype=np.int64)
+    L = len(k_pools)
+    nt = len(trig)
+    H = p["n_kv_heads"]
+    W, U, bs = p["window"], p["buffer"], p["block_size"]
+    N = W - U
+    nw = int(n_windows)
+    budget, alpha, gamma = p["budget"], p["chunk_budget"], p["max_chunk_len"]
+    # the windows together span (nw-1)*N + W positions from p0
+    status = validate(dict(p, window=(nw - 1) * N + W), trig, block_table, seq_lens, win_start)
+
+    scores = np.zeros((L, nt, nw, H, N), dtype=np.float32)
+    disc = np.zeros((L, nt, nw, H, budget - alpha), dtype=np.int32)
+    kept = np.zeros((L, nt, nw, H, budget), dtype=np.int32)
+    if score_override is not None:
+        scores[...] = score_override
+    else:
+        for w in range(nw):
+            starts = np.asarray(win_start, dtype=np.int64) + w * N
+            units = [(l, t, h) for l in range(L) for t in range(nt) for h in range(H) if status[t] == 0]
+            res = score_units(p, trig, q_raw[:, :, w], k_pools, block_table, starts, units, threads)
+            for (l, t, h), a in zip(units, res):
+                scores[l, t, w, h] = round_scores(a)
+    for l in range(L):
+        for t in range(nt):
+            for w in range(nw):
+                for h in range(H):
+                    d_, k_ = kept_set(scores[l, t, w, h], budget, alpha, gamma)
+                    disc[l, t, w, h] = d_
+                    kept[l, t, w, h] = k_
+
+    freed, n_freed = [], np.zeros(nt, dtype=np.int32)
+    for t in range(nt):
+        if status[t] != 0:
+            freed.append([])
+            continue
+        s = int(trig[t])
+        p0, sl = int(win_start[s]), int(seq_lens[s])
+        pos = window_positions(p0, sl - p0)
+        for l in range(L):
+            for pool in (k_pools[l], v_pools[l]):
+                for h in range(H):
+                    before = read_rows(pool, block_table[s], pos, h, bs)
+                    parts = [before[w * N + kept[l, t, w, h]] for w in range(nw)] + [before[nw * N:]]
+                    after = np.concatenate(parts)
+                    write_rows(pool, block_table[s], pos[:after.shape[0]], h, bs, after)
+        if commit:
+            new_len = sl - nw * (N - budget)
             blocks = released_blocks(sl, new_len, bs)
             freed.append([int(block_table[s, b]) for b in blocks])
             n_freed[t] = len(blocks)

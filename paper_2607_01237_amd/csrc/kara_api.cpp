@@ -40,6 +40,7 @@ kara_status_t make_geom(const kara_params_t* p, int32_t n_trig, Geom* g) {
   g->U = U;
   g->N = N;
   g->Wq = p->score_queries > 0 ? p->score_queries : W;
+  g->n_win = 1;
   g->budget = p->budget;
   g->alpha = p->chunk_budget;
   g->gamma = p->max_chunk_len;
@@ -87,7 +88,7 @@ struct WsLayout {
 };
 
 WsLayout ws_layout(const Geom& g, int n_layers, const ScorePlan& sp) {
-  const int64_t units = (int64_t)n_layers * g.n_trig * g.Hkv;
+  const int64_t units = (int64_t)n_layers * g.n_trig * g.n_win * g.Hkv;
   WsLayout w{};
   size_t off = 0;
   w.partials = off;
@@ -127,8 +128,8 @@ hipError_t run_score(const Geom& g, const ScorePlan& sp, int n_layers, const voi
                      const void* const* k_pools, const int32_t* trig, const int32_t* bt,
                      const int32_t* win_start, const int32_t* status, float* partials,
                      float* scores, hipStream_t stream) {
-  const int64_t q_layer = (int64_t)g.n_trig * g.Wq * g.Hq * g.d * g.esize;
-  const int64_t units_layer = (int64_t)g.n_trig * g.Hkv;
+  const int64_t q_layer = (int64_t)g.n_trig * g.n_win * g.Wq * g.Hq * g.d * g.esize;
+  const int64_t units_layer = (int64_t)g.n_trig * g.n_win * g.Hkv;
   return for_layer_chunks(n_layers, k_pools, nullptr, [&](int l0, int cnt, const PoolPtrs& kp, const PoolPtrs&) {
     return launch_score(g, sp, cnt, (const char*)q + l0 * q_layer, kp, trig, bt, win_start, status,
                         partials + l0 * units_layer * sp.n_splits * g.N, scores + l0 * units_layer * g.N,
@@ -140,12 +141,56 @@ hipError_t run_compact(const Geom& g, int n_layers, const int32_t* trig, const i
                        void* const* k_pools, void* const* v_pools, const int32_t* bt,
                        const int32_t* seq_lens, const int32_t* win_start, const int32_t* status,
                        hipStream_t stream) {
-  const int64_t k_layer = (int64_t)g.n_trig * g.Hkv * g.budget;
+  const int64_t k_layer = (int64_t)g.n_trig * g.n_win * g.Hkv * g.budget;
   return for_layer_chunks(n_layers, (const void* const*)k_pools, (const void* const*)v_pools,
                           [&](int l0, int cnt, const PoolPtrs& kp, const PoolPtrs& vp) {
                             return launch_compact(g, cnt, trig, kept + l0 * k_layer, kp, vp, bt,
                                                   seq_lens, win_start, status, stream);
                           });
+}
+
+// One compression event over n_win consecutive windows (stride W - U) of
+// each listed sequence: validation, scoring, selection, compaction and, if
+// asked, the metadata commit.
+kara_status_t compress(const kara_params_t* p, int32_t n_trig, const int32_t* trig, int32_t n_win,
+                       int32_t n_layers, const void* q, void* const* k_pools, void* const* v_pools,
+                       int32_t* block_table, int32_t* seq_lens, const int32_t* win_start, int32_t commit,
+                       float* scores, int32_t* discrete, int32_t* kept, int32_t* freed, int32_t* n_freed,
+                       int32_t* status, void* workspace, size_t workspace_bytes, void* stream) {
+  Geom g;
+  kara_status_t st = make_geom(p, n_trig, &g);
+  if (st != KARA_OK) return st;
+  if (n_layers < 1 || n_win < 1) return KARA_ERR_INVALID_ARG;
+  if ((int64_t)(n_win - 1) * g.N + g.W > (int64_t)g.max_blocks * g.bs) return KARA_ERR_INVALID_ARG;
+  g.n_win = n_win;
+  if (n_trig == 0) return KARA_OK;
+  if (!trig || !q || !block_table || !seq_lens || !win_start || !status ||
+      !pools_ok((const void* const*)k_pools, n_layers) || !pools_ok((const void* const*)v_pools, n_layers))
+    return KARA_ERR_INVALID_ARG;
+  if (commit && (!freed || !n_freed)) return KARA_ERR_INVALID_ARG;
+  const int64_t units = (int64_t)n_layers * n_trig * n_win * g.Hkv;
+  if (units > INT32_MAX) return KARA_ERR_INVALID_ARG;
+  const ScorePlan sp = plan_score(g, units);
+  const WsLayout wl = ws_layout(g, n_layers, sp);
+  if (!workspace || workspace_bytes < wl.total) return KARA_ERR_WORKSPACE;
+  char* ws = (char*)workspace;
+  float* partials = (float*)(ws + wl.partials);
+  float* scores_buf = scores ? scores : (float*)(ws + wl.scores);
+  int32_t* kept_buf = kept ? kept : (int32_t*)(ws + wl.kept);
+  hipStream_t s = (hipStream_t)stream;
+
+  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, s);
+  if (e == hipSuccess)
+    e = run_score(g, sp, n_layers, q, (const void* const*)k_pools, trig, block_table, win_start, status,
+                  partials, scores_buf, s);
+  if (e == hipSuccess)
+    e = launch_select(g, units, kSelectDiscrete | kSelectKept, scores_buf, nullptr, discrete, kept_buf, s);
+  if (e == hipSuccess)
+    e = run_compact(g, n_layers, trig, kept_buf, k_pools, v_pools, block_table, seq_lens, win_start,
+                    status, s);
+  if (e == hipSuccess && commit)
+    e = launch_commit(g, trig, block_table, seq_lens, win_start, freed, n_freed, status, s);
+  return hip_status(e);
 }
 
 }  // namespace
@@ -286,38 +331,19 @@ kara_status_t kara_compress_window(const kara_params_t* p, int32_t n_trig, const
                                    int32_t* discrete, int32_t* kept, int32_t* freed,
                                    int32_t* n_freed, int32_t* status, void* workspace,
                                    size_t workspace_bytes, void* stream) {
-  Geom g;
-  kara_status_t st = make_geom(p, n_trig, &g);
-  if (st != KARA_OK) return st;
-  if (n_layers < 1) return KARA_ERR_INVALID_ARG;
-  if (n_trig == 0) return KARA_OK;
-  if (!trig || !q || !block_table || !seq_lens || !win_start || !status ||
-      !pools_ok((const void* const*)k_pools, n_layers) || !pools_ok((const void* const*)v_pools, n_layers))
-    return KARA_ERR_INVALID_ARG;
-  if (commit && (!freed || !n_freed)) return KARA_ERR_INVALID_ARG;
-  const int64_t units = (int64_t)n_layers * n_trig * g.Hkv;
-  if (units > INT32_MAX) return KARA_ERR_INVALID_ARG;
-  const ScorePlan sp = plan_score(g, units);
-  const WsLayout wl = ws_layout(g, n_layers, sp);
-  if (!workspace || workspace_bytes < wl.total) return KARA_ERR_WORKSPACE;
-  char* ws = (char*)workspace;
-  float* partials = (float*)(ws + wl.partials);
-  float* scores_buf = scores ? scores : (float*)(ws + wl.scores);
-  int32_t* kept_buf = kept ? kept : (int32_t*)(ws + wl.kept);
-  hipStream_t s = (hipStream_t)stream;
+  return compress(p, n_trig, trig, 1, n_layers, q, k_pools, v_pools, block_table, seq_lens, win_start, commit,
+                  scores, discrete, kept, freed, n_freed, status, workspace, workspace_bytes, stream);
+}
 
-  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, s);
-  if (e == hipSuccess)
-    e = run_score(g, sp, n_layers, q, (const void* const*)k_pools, trig, block_table, win_start, status,
-                  partials, scores_buf, s);
-  if (e == hipSuccess)
-    e = launch_select(g, units, kSelectDiscrete | kSelectKept, scores_buf, nullptr, discrete, kept_buf, s);
-  if (e == hipSuccess)
-    e = run_compact(g, n_layers, trig, kept_buf, k_pools, v_pools, block_table, seq_lens, win_start,
-                    status, s);
-  if (e == hipSuccess && commit)
-    e = launch_commit(g, trig, block_table, seq_lens, win_start, freed, n_freed, status, s);
-  return hip_status(e);
+kara_status_t kara_compress_prefill(const kara_params_t* p, int32_t n_trig, const int32_t* trig,
+                                    int32_t n_windows, int32_t n_layers, const void* q,
+                                    void* const* k_pools, void* const* v_pools, int32_t* block_table,
+                                    int32_t* seq_lens, const int32_t* win_start, int32_t commit,
+                                    float* scores, int32_t* discrete, int32_t* kept, int32_t* freed,
+                                    int32_t* n_freed, int32_t* status, void* workspace,
+                                    size_t workspace_bytes, void* stream) {
+  return compress(p, n_trig, trig, n_windows, n_layers, q, k_pools, v_pools, block_table, seq_lens, win_start,
+                  commit, scores, discrete, kept, freed, n_freed, status, workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

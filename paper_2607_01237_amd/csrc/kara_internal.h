@@ -16,6 +16,8 @@ constexpr int kMaxLayersPerLaunch = 64;
 struct Geom {
   int W, U, N;          // window, buffer, compressible length N = W - U
   int Wq;               // scoring queries per unit (the window's last Wq positions)
+  int n_win;            // windows per listed sequence: 1, or consecutive prefill windows
+                        // at stride N (units = layers x n_trig x n_win x Hkv)
   int budget, alpha, gamma;
   int k_disc;           // budget - alpha, Eq. (5)
   int n_chunks;         // floor(alpha / (gamma - 2)), Eq. (7)

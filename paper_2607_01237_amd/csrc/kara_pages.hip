@@ -25,7 +25,9 @@ __global__ void validate_kernel(Geom g, const int32_t* __restrict__ trig,
     }
   const int p0 = win_start[s];
   const int len = seq_lens[s];
-  if (p0 < 0 || (int64_t)p0 + g.W > (int64_t)len || (int64_t)len > (int64_t)g.max_blocks * g.bs) {
+  // the windows cover [p0, p0 + (n_win-1)*N + W)
+  if (p0 < 0 || (int64_t)p0 + (int64_t)(g.n_win - 1) * g.N + g.W > (int64_t)len ||
+      (int64_t)len > (int64_t)g.max_blocks * g.bs) {
     status[t] = st | KARA_SEQ_BAD_WINDOW;
     return;
   }
@@ -42,11 +44,12 @@ __global__ void validate_kernel(Geom g, const int32_t* __restrict__ trig,
 }
 
 // Flags triggered sequences whose kept rows (caller-supplied) are not a
-// strictly ascending subset of [0, N); one workgroup per unit.
+// strictly ascending subset of [0, N); one workgroup per unit
+// ((layer, trigger, window, head)).
 __global__ void check_kept_kernel(Geom g, int n_layers, const int32_t* __restrict__ kept,
                                   int32_t* __restrict__ status) {
   const int64_t u = blockIdx.x;
-  const int t = (int)((u / g.Hkv) % g.n_trig);
+  const int t = (int)((u / ((int64_t)g.Hkv * g.n_win)) % g.n_trig);
   const int32_t* kr = kept + u * g.budget;
   int bad = 0;
   for (int j = threadIdx.x; j < g.budget; j += blockDim.x) {
@@ -59,11 +62,14 @@ __global__ void check_kept_kernel(Geom g, int n_layers, const int32_t* __restric
 constexpr int kCompactThreads = 256;
 constexpr int kCompactUnroll = 4;
 
-// One workgroup per (unit, K|V).  Destination row j (window-relative) takes
-// source row m(j): kept[j] for j < budget, then the buffer rows W-U.., then
-// the tail rows W..  m is strictly increasing with m(j) >= j, so processing
-// destination tiles in ascending order -- every source of a tile loaded
-// before any row of it is stored -- never overwrites a row still to be read.
+// One workgroup per ((layer, trigger, head), K|V).  Destination row j
+// (relative to the first window's start p0) takes source row m(j): for the
+// n_win windows in turn (window w's compressible rows start at w*N) its kept
+// rows w*N + kept_w[.], then everything after the last window's compressible
+// region -- its buffer and the tail -- in order.  (One window: kept, buffer,
+// tail.)  m is strictly increasing with m(j) >= j, so processing destination
+// tiles in ascending order -- every source of a tile loaded before any row of
+// it is stored -- never overwrites a row still to be read.
 __global__ __launch_bounds__(kCompactThreads) void compact_kernel(
     Geom g, const int32_t* __restrict__ trig, const int32_t* __restrict__ kept, PoolPtrs kp,
     PoolPtrs vp, const int32_t* __restrict__ bt, const int32_t* __restrict__ seq_lens,
@@ -77,9 +83,12 @@ __global__ __launch_bounds__(kCompactThreads) void compact_kernel(
   if (status[t] != 0) return;
   const int s = trig[t];
   const int p0 = win_start[s];
-  const int tail = seq_lens[s] - p0 - g.W;
-  const int n_dst = g.budget + g.U + tail;
-  const int32_t* __restrict__ kr = kept + u * g.budget;
+  const int kept_rows = g.n_win * g.budget;
+  const int comp_rows = g.n_win * g.N;
+  const int n_dst = seq_lens[s] - p0 - (comp_rows - kept_rows);
+  // kept rows of window w: kr + w * Hkv * budget ([l][t][w][h][budget])
+  const int32_t* __restrict__ kr = kept + (((int64_t)l * g.n_trig + t) * g.n_win * g.Hkv + h) * g.budget;
+  const int64_t kr_win = (int64_t)g.Hkv * g.budget;
   char* base = (char*)(kv ? vp.p[l] : kp.p[l]);
   const int32_t* __restrict__ row_pages = bt + (int64_t)s * g.max_blocks;
   const int row_bytes = g.d * g.esize;
@@ -103,8 +112,13 @@ __global__ __launch_bounds__(kCompactThreads) void compact_kernel(
       const int j = x0 + k * rpp + r;
       dst[k] = -1;
       if (j < n_dst) {
-        const int src = j < g.budget ? kr[j]
-                                     : (j < g.budget + g.U ? g.N + (j - g.budget) : g.W + (j - g.budget - g.U));
+        int src;
+        if (j < kept_rows) {
+          const int w = g.n_win == 1 ? 0 : j / g.budget;
+          src = w * g.N + kr[w * kr_win + (j - w * g.budget)];
+        } else {
+          src = comp_rows + (j - kept_rows);
+        }
         if (src != j) {
           dst[k] = j;
           v[k] = *(const uint4*)row_addr(src);
@@ -133,7 +147,7 @@ __global__ void commit_kernel(Geom g, const int32_t* __restrict__ trig, int32_t*
   }
   const int s = trig[t];
   const int len = seq_lens[s];
-  const int new_len = len - (g.N - g.budget);
+  const int new_len = len - g.n_win * (g.N - g.budget);
   const int old_b = (len + g.bs - 1) / g.bs;
   const int new_b = (new_len + g.bs - 1) / g.bs;
   int32_t* row = bt + (int64_t)s * g.max_blocks;
@@ -161,7 +175,7 @@ hipError_t launch_validate(const Geom& g, const int32_t* trig, const int32_t* bl
 
 hipError_t launch_check_kept(const Geom& g, int n_layers, const int32_t* kept, int32_t* status,
                              hipStream_t stream) {
-  const int64_t units = (int64_t)n_layers * g.n_trig * g.Hkv;
+  const int64_t units = (int64_t)n_layers * g.n_trig * g.n_win * g.Hkv;
   hipLaunchKernelGGL(check_kept_kernel, dim3((unsigned)units), dim3(256), 0, stream, g, n_layers,
                      kept, status);
   return hipGetLastError();

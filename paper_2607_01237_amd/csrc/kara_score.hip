@@ -215,9 +215,13 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
   if ((a.n_blocks & 7) == 0) bid = (bid & 7) * (a.n_blocks >> 3) + (bid >> 3);
   const int64_t u = bid / a.n_splits;
   const int split = (int)(bid % a.n_splits);
+  // unit u = ((l * n_trig + t) * n_win + w) * Hkv + h; window w of the
+  // trigger starts w*N after win_start
   const int h = (int)(u % g.Hkv);
-  const int t = (int)((u / g.Hkv) % g.n_trig);
-  const int l = (int)(u / ((int64_t)g.Hkv * g.n_trig));
+  const int tw = (int)((u / g.Hkv) % ((int64_t)g.n_trig * g.n_win));
+  const int t = tw / g.n_win;
+  const int wi = tw - t * g.n_win;
+  const int l = (int)(u / ((int64_t)g.Hkv * g.n_trig * g.n_win));
   const int N = g.N;
   const int nch = (N + kChunkKeys - 1) / kChunkKeys;
   float* out = a.n_splits == 1 ? a.scores + u * (int64_t)N : a.partials + (u * a.n_splits + split) * (int64_t)N;
@@ -227,9 +231,9 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
     return;
   }
   const int s = a.trig[t];
-  const int p0 = a.win_start[s];
+  const int p0 = a.win_start[s] + wi * N;
   const char* kpool = (const char*)a.k.p[l];
-  const char* qunit = a.q + ((int64_t)l * g.n_trig + t) * g.Wq * g.Hq * (int64_t)C::kRowBytes;
+  const char* qunit = a.q + (((int64_t)l * g.n_trig + t) * g.n_win + wi) * g.Wq * g.Hq * (int64_t)C::kRowBytes;
   const int R = g.G * g.Wq;
   const float c = g.scale * kLog2e;
 
@@ -626,7 +630,7 @@ hipError_t launch_score(const Geom& g, const ScorePlan& sp, int n_layers, const 
   a.partials = partials;
   a.scores = scores;
   a.n_splits = sp.n_splits;
-  a.n_blocks = (int64_t)n_layers * g.n_trig * g.Hkv * sp.n_splits;
+  a.n_blocks = (int64_t)n_layers * g.n_trig * g.n_win * g.Hkv * sp.n_splits;
   if (a.n_blocks == 0) return hipSuccess;
   const int rt = sp.rows_wg / (kScoreWaves * 16);
   hipError_t e;

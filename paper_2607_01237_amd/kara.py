@@ -77,6 +77,8 @@ _SIGS = {
     "kara_commit_tables": (_I32, [_PAR, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     "kara_compress_window": (_I32, [_PAR, _I32, _VP, _I32, _VP, _PP, _PP, _VP, _VP, _VP, _I32, _VP, _VP,
                                     _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP]),
+    "kara_compress_prefill": (_I32, [_PAR, _I32, _VP, _I32, _I32, _VP, _PP, _PP, _VP, _VP, _VP, _I32, _VP, _VP,
+                                     _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP]),
     "kara_harness_kv_append": (_I32, [_PAR, _I32, _VP, _I32, _I32, _VP, _VP, _PP, _PP, _VP, _VP, _VP, _VP]),
     "kara_harness_decode_workspace_size": (_I32, [_PAR, _I32, _I32, _I32, ctypes.POINTER(ctypes.c_size_t)]),
     "kara_harness_decode_attention": (_I32, [_PAR, _I32, _VP, _I32, _VP, _PP, _PP, _VP, _VP, _I32, _VP, _VP,
@@ -202,6 +204,17 @@ def compress_window(p, trig, q, k_pools, v_pools, block_table, seq_lens, win_sta
                     workspace, scores=None, discrete=None, kept=None, freed=None, n_freed=None, stream=None):
     _check("kara_compress_window", load().kara_compress_window(
         ctypes.byref(p), trig.numel(), _ptr(trig), len(k_pools), _ptr(q), _ptr_array(k_pools),
+        _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), _ptr(win_start), int(bool(commit)),
+        _ptr(scores), _ptr(discrete), _ptr(kept), _ptr(freed), _ptr(n_freed), _ptr(status), _ptr(workspace),
+        workspace.numel() * workspace.element_size() if workspace is not None else 0, _stream(stream)))
+
+
+
+def compress_prefill(p, trig, n_windows, q, k_pools, v_pools, block_table, seq_lens, win_start, commit, status,
+                     workspace, scores=None, discrete=None, kept=None, freed=None, n_freed=None, stream=None):
+    """n_windows consecutive windows of every listed sequence at once (App. C.2)."""
+    _check("kara_compress_prefill", load().kara_compress_prefill(
+        ctypes.byref(p), trig.numel(), _ptr(trig), int(n_windows), len(k_pools), _ptr(q), _ptr_array(k_pools),
         _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), _ptr(win_start), int(bool(commit)),
         _ptr(scores), _ptr(discrete), _ptr(kept), _ptr(freed), _ptr(n_freed), _ptr(status), _ptr(workspace),
         workspace.numel() * workspace.element_size() if workspace is not None else 0, _stream(stream)))
