@@ -14,12 +14,13 @@ import re
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libkara.so")
-HEADERS = [os.path.join(os.path.dirname(_PKG), "include", h) for h in ("kara.h", "kara_harness.h")]
+HEADERS = [os.path.join(os.path.dirname(_PKG), "include", h) for h in ("kara.h", "kara_harness.h", "kara_sched.h")]
 
 BF16, F32 = 0, 1
-OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, -1, -2, -3, -4
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_SCHED_MISMATCH = 0, -1, -2, -3, -4, -5
 SEQ_OK, SEQ_BAD_WINDOW, SEQ_BAD_PAGE, SEQ_DUP_TRIGGER, SEQ_BAD_INDEX, SEQ_BAD_KEPT = 0, 1, 2, 4, 8, 16
 MAX_COMPRESSIBLE = 4096
+REQ_WAITING, REQ_RUNNING, REQ_FINISHED = 0, 1, 2
 
 
 class KaraError(RuntimeError):
@@ -46,6 +47,38 @@ class KaraParams(ctypes.Structure):
         ("scale", ctypes.c_float),
         ("score_queries", ctypes.c_int32),
     ]
+
+
+class SchedConfig(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "n_slots", "num_pages", "block_size", "max_blocks_per_seq", "window", "buffer", "budget", "period",
+        "max_per_event", "max_running", "reserve_pages", "compress", "protect_prompt")]
+
+
+_P32 = ctypes.POINTER(ctypes.c_int32)
+_P64 = ctypes.POINTER(ctypes.c_int64)
+
+
+class SchedStep(ctypes.Structure):
+    _fields_ = [("n_preempted", ctypes.c_int32), ("preempted", _P32), ("n_decode", ctypes.c_int32),
+                ("decode", _P32), ("n_admitted", ctypes.c_int32), ("admitted", _P32), ("prefill_len", _P32),
+                ("admitted_id", _P64), ("tables_changed", ctypes.c_int32)]
+
+
+class SchedEvent(ctypes.Structure):
+    _fields_ = [("n_trig", ctypes.c_int32), ("trig", _P32), ("win_start", _P32)]
+
+
+class SchedStats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in ("steps", "events", "compressed", "pages_reclaimed", "preemptions",
+                                              "tokens_decoded", "tokens_prefilled")] + \
+               [(n, ctypes.c_int32) for n in ("running", "waiting", "finished", "free_pages", "peak_running",
+                                              "pages_in_use")]
+
+
+class SchedRequest(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("state", "slot", "len", "win_start", "generated", "compressions",
+                                              "preemptions")]
 
 
 def make_params(p: dict, n_seqs: int) -> KaraParams:
@@ -83,6 +116,15 @@ _SIGS = {
     "kara_harness_decode_workspace_size": (_I32, [_PAR, _I32, _I32, _I32, ctypes.POINTER(ctypes.c_size_t)]),
     "kara_harness_decode_attention": (_I32, [_PAR, _I32, _VP, _I32, _VP, _PP, _PP, _VP, _VP, _I32, _VP, _VP,
                                              ctypes.c_size_t, _VP]),
+    "kara_sched_create": (_I32, [ctypes.POINTER(SchedConfig), _P32, ctypes.POINTER(ctypes.c_void_p)]),
+    "kara_sched_destroy": (_I32, [_VP]),
+    "kara_sched_submit": (_I32, [_VP, _I32, _I32, _P64]),
+    "kara_sched_step_begin": (_I32, [_VP, ctypes.POINTER(SchedStep)]),
+    "kara_sched_step_end": (_I32, [_VP, ctypes.POINTER(SchedEvent)]),
+    "kara_sched_event_commit": (_I32, [_VP, _P32, _P32]),
+    "kara_sched_tables": (_I32, [_VP, ctypes.POINTER(_P32), ctypes.POINTER(_P32)]),
+    "kara_sched_stats": (_I32, [_VP, ctypes.POINTER(SchedStats)]),
+    "kara_sched_request": (_I32, [_VP, ctypes.c_int64, ctypes.POINTER(SchedRequest)]),
 }
 
 _lib = None
@@ -244,3 +286,96 @@ def decode_attention(p, seqs, q, k_pools, v_pools, block_table, seq_lens, max_le
         ctypes.byref(p), seqs.numel(), _ptr(seqs), len(k_pools), _ptr(q), _ptr_array(k_pools),
         _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), max_len, _ptr(out), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+# ---- periodic compression policy (include/kara_sched.h): host runtime
+
+def _host_i32(a):
+    """Host int32 pointer of a contiguous numpy array (or None)."""
+    import numpy as np
+    if a is None:
+        return None
+    a = np.ascontiguousarray(a, dtype=np.int32)
+    return a, a.ctypes.data_as(_P32)
+
+
+def _view(ptr, n, dtype):
+    import numpy as np
+    if n <= 0:
+        return np.zeros(0, dtype=dtype)
+    return np.ctypeslib.as_array(ptr, shape=(n,)).copy()
+
+
+class Scheduler:
+    """The host scheduler of include/kara_sched.h; every decision is made by
+    the library, this class only converts its outputs to numpy arrays."""
+
+    CONFIG_DEFAULTS = dict(reserve_pages=0, compress=1, protect_prompt=0)
+
+    def __init__(self, cfg: dict, page_order=None):
+        import numpy as np
+        vals = dict(self.CONFIG_DEFAULTS, **cfg)
+        self.cfg = SchedConfig(**{name: int(vals[name]) for name, _ in SchedConfig._fields_})
+        self._lib = load()
+        self._h = ctypes.c_void_p()
+        po = _host_i32(page_order)
+        _check("kara_sched_create", self._lib.kara_sched_create(ctypes.byref(self.cfg), po[1] if po else None,
+                                                                  ctypes.byref(self._h)))
+        self.n_slots, self.max_blocks = self.cfg.n_slots, self.cfg.max_blocks_per_seq
+        self._np = np
+
+    def close(self):
+        if self._h:
+            self._lib.kara_sched_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def submit(self, prompt_len: int, max_new: int) -> int:
+        rid = ctypes.c_int64(-1)
+        _check("kara_sched_submit", self._lib.kara_sched_submit(self._h, int(prompt_len), int(max_new),
+                                                                  ctypes.byref(rid)))
+        return int(rid.value)
+
+    def step_begin(self) -> dict:
+        st = SchedStep()
+        _check("kara_sched_step_begin", self._lib.kara_sched_step_begin(self._h, ctypes.byref(st)))
+        i32, i64 = self._np.int32, self._np.int64
+        return dict(preempted=_view(st.preempted, st.n_preempted, i32), decode=_view(st.decode, st.n_decode, i32),
+                    admitted=_view(st.admitted, st.n_admitted, i32),
+                    prefill_len=_view(st.prefill_len, st.n_admitted, i32),
+                    admitted_id=_view(st.admitted_id, st.n_admitted, i64), tables_changed=bool(st.tables_changed))
+
+    def step_end(self):
+        """(triggered slots, window start of every slot)."""
+        ev = SchedEvent()
+        _check("kara_sched_step_end", self._lib.kara_sched_step_end(self._h, ctypes.byref(ev)))
+        return _view(ev.trig, ev.n_trig, self._np.int32), _view(ev.win_start, self.n_slots, self._np.int32)
+
+    def commit(self, freed=None, n_freed=None):
+        """Applies the pending event; freed / n_freed (host arrays) are checked
+        against the scheduler's own release when given."""
+        f, n = _host_i32(freed), _host_i32(n_freed)
+        _check("kara_sched_event_commit", self._lib.kara_sched_event_commit(self._h, f[1] if f else None,
+                                                                              n[1] if n else None))
+
+    def tables(self):
+        """Copies of the host block table [n_slots, max_blocks] and lengths [n_slots]."""
+        bt, ln = _P32(), _P32()
+        _check("kara_sched_tables", self._lib.kara_sched_tables(self._h, ctypes.byref(bt), ctypes.byref(ln)))
+        return (_view(bt, self.n_slots * self.max_blocks, self._np.int32).reshape(self.n_slots, self.max_blocks),
+                _view(ln, self.n_slots, self._np.int32))
+
+    def stats(self) -> dict:
+        s = SchedStats()
+        _check("kara_sched_stats", self._lib.kara_sched_stats(self._h, ctypes.byref(s)))
+        return {name: int(getattr(s, name)) for name, _ in SchedStats._fields_}
+
+    def request(self, rid: int) -> dict:
+        r = SchedRequest()
+        _check("kara_sched_request", self._lib.kara_sched_request(self._h, int(rid), ctypes.byref(r)))
+        return {name: int(getattr(r, name)) for name, _ in SchedRequest._fields_}
