@@ -18,11 +18,15 @@ sample of units on this host.
 
     python bench.py [--steps K] [--warmup W] [--workload qwen14b|batch8|ragged|buffer_only|threshold_topk|prefill]
     python bench.py --workload soak [--intervals n] [--warmup W]
+    python bench.py --workload serve [--requests n]
 
 The soak runs the compression step inside a decode loop (append, decode
 attention, compress, reclaim pages; paper_2607_01237_amd/soak.py) and reports
 per-event compression latency, per-step decode latency and pages reclaimed;
-its `value` averages the events after the first W.
+its `value` averages the events after the first W.  The serve workload runs
+a batch of requests through the periodic policy's serving loop
+(paper_2607_01237_amd/serve.py) with and without compression on the same
+memory-bound pool and reports generated tokens/s of each.
 """
 
 from __future__ import annotations
@@ -52,6 +56,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--intervals", type=int, default=0, help="soak only: number of compression intervals "
                                                              "(default: the workload's 31)")
+    ap.add_argument("--requests", type=int, default=0, help="serve only: number of requests (default: the "
+                                                           "workload's 128)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="rough budget of the CPU-oracle sample")
     ap.add_argument("--copy-calibration-gib", type=float, default=0.0,
                     help="run one plain streaming kernel (bf16 negation) over this many GiB before the steps, as "
@@ -394,6 +400,79 @@ def run_soak(args):
     print(json.dumps(result), flush=True)
 
 
+def run_serve(args):
+    """The serving analogue of the paper's throughput runs (App. B.1): a batch
+    of requests served to completion by the periodic policy on a memory-bound
+    pool, then by the same loop with compression switched off (the
+    uncompressed baseline), same requests and pool.  Reports generated tokens
+    per second of each, mean concurrency and preemptions."""
+    import torch
+
+    import kara_inputs as ki
+    from paper_2607_01237_amd import kara
+    from paper_2607_01237_amd.serve import Serve
+
+    kara.load()
+    device = torch.device("cuda:0")
+    torch.cuda.set_device(device)
+    over = {"n_requests": args.requests} if args.requests else {}
+    shape, sc, prompts, gens, order = ki.serve_setup(**over)
+    runs = {}
+    for comp in (1, 0):
+        srv = Serve(shape, dict(sc, compress=comp), device, ki.SERVE["seed"], page_order=order)
+        for p_, g_ in zip(prompts, gens):
+            srv.submit(int(p_), int(g_))
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        steps, chunk = 0, 500
+        while True:
+            done = srv.run(chunk)
+            steps += done
+            st = srv.sched.stats()
+            log(f"serve compress={comp}: {steps} steps, finished {st['finished']}/{len(prompts)}, running "
+                f"{st['running']}, events {st['events']}, preemptions {st['preemptions']}, "
+                f"{time.perf_counter() - t0:.0f} s")
+            if st["finished"] == len(prompts) or steps >= 50000:
+                break
+        srv.verify()
+        wall = time.perf_counter() - t0
+        st = srv.sched.stats()
+        hist = np.array(srv.history)
+        runs[comp] = dict(steps=steps, wall_s=wall, tokens_decoded=st["tokens_decoded"],
+                          tokens_per_s=st["tokens_decoded"] / wall, ms_per_step=wall * 1e3 / steps,
+                          mean_running=float(hist[:, 0].mean()), peak_running=st["peak_running"],
+                          preemptions=st["preemptions"], tokens_prefilled=st["tokens_prefilled"],
+                          events=st["events"], sequences_compressed=st["compressed"],
+                          pages_reclaimed=st["pages_reclaimed"], finished=st["finished"])
+        del srv
+        torch.cuda.empty_cache()
+    on, off = runs[1], runs[0]
+    page_gb = 2 * shape["n_layers"] * shape["n_kv_heads"] * sc["block_size"] * shape["head_dim"] * 2 / 1e9
+    result = {
+        "metric": "generated tokens/s, serving loop under the periodic compression policy (synthetic tokens)",
+        "value": on["tokens_per_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": on["steps"],
+        "warmup": 0,
+        "ms_per_step": on["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": shape["dtype"],
+        "data": "synthetic (seeded N(0,1) K/V and queries; no model weights, datasets or sampling)",
+        "config": {
+            "workload": "serve", "requests": len(prompts), "layers": shape["n_layers"],
+            "q_heads": shape["n_q_heads"], "kv_heads": shape["n_kv_heads"], "head_dim": shape["head_dim"],
+            "prompt_range": list(ki.SERVE["prompt"]), "gen_range": list(ki.SERVE["gen"]),
+            "pool_pages": sc["num_pages"], "pool_GB": sc["num_pages"] * page_gb, **{k: sc[k] for k in (
+                "block_size", "window", "buffer", "budget", "period", "max_per_event", "max_running")},
+        },
+        "serve": {"kara": on, "uncompressed": off, "speedup": on["tokens_per_s"] / off["tokens_per_s"]},
+    }
+    print(json.dumps(result), flush=True)
+
+
 def main():
     args = parse()
     if args.summarize_pmc:
@@ -406,6 +485,9 @@ def main():
         sys.exit(2)
     if args.workload == "soak":
         run_soak(args)
+        return
+    if args.workload == "serve":
+        run_serve(args)
         return
     import torch
 

@@ -198,6 +198,42 @@ def soak_geometry(cfg: dict) -> SoakGeometry:
                         free_list=rng.permutation(num_pages).astype(np.int32))
 
 
+# ---------------------------------------------------------------- serving
+# The serving analogue of the paper's KvLLM runs (App. B.1): an 8B-class
+# decoder (32 layers, 32/8 heads, d=128, bf16), 256-token blocks, windows of
+# three blocks (768) with a 32-token buffer, 257 tokens retained per window
+# (budget 225 plus the buffer), an event every 128 steps compressing at most
+# 30 sequences.  A batch of requests with short prompts and reasoning-length
+# generations arrives at once, against a pool that holds about 37 % of what
+# the batch would need uncompressed, so admission is memory bound.
+SERVE = dict(
+    shape=dict(n_layers=32, n_q_heads=32, n_kv_heads=8, head_dim=128, dtype="bf16", chunk_budget=16,
+               max_chunk_len=8),
+    sched=dict(n_slots=256, block_size=256, window=768, buffer=32, budget=225, period=128, max_per_event=30,
+               max_running=256, reserve_pages=4, protect_prompt=0),
+    n_requests=128, prompt=(64, 256), gen=(1024, 3072), pool_frac=0.37, seed=8,
+)
+
+
+def serve_setup(cfg: dict = None, **over):
+    """(shape, scheduler config without `compress`, prompts, generation
+    lengths, initial free list) of a serving run.  Lengths are uniform in the
+    stated closed ranges; the pool is pool_frac of the batch's uncompressed
+    demand, rounded up to whole pages."""
+    c = copy.deepcopy(SERVE if cfg is None else cfg)
+    c.update(over)
+    rng = np.random.default_rng(c["seed"])
+    n = c["n_requests"]
+    prompts = rng.integers(c["prompt"][0], c["prompt"][1] + 1, n).astype(np.int32)
+    gens = rng.integers(c["gen"][0], c["gen"][1] + 1, n).astype(np.int32)
+    sc = dict(c["sched"])
+    bs = sc["block_size"]
+    sc["max_blocks_per_seq"] = _blocks(int((prompts + gens).max()), bs)
+    sc["num_pages"] = _blocks(int(np.ceil(c["pool_frac"] * float((prompts + gens).sum()))), bs)
+    order = rng.permutation(sc["num_pages"]).astype(np.int32)
+    return dict(c["shape"]), sc, prompts, gens, order
+
+
 # ---------------------------------------------------------------- tensors
 def torch_dtype(cfg):
     import torch

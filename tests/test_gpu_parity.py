@@ -144,3 +144,10 @@ def test_threshold_topk_baseline():
     # window, its last 32 tokens score and are kept, plain top-k of 993
     case, rep, gpu = _run(ki.workload("threshold_topk", n_seqs=3, n_layers=2))
     assert (gpu["seq_lens"][case.geom.trig] == 1025).all()
+
+
+def test_kvllm_serving_geometry():
+    # the serving runs' geometry (App. B.1): 256-token blocks, a window of
+    # three blocks with a 32-token buffer, 225 kept + 32 buffer = 257 retained
+    _run(ki.workload("batch8", n_seqs=3, n_layers=2, block_size=256, window=768, buffer=32, budget=225,
+                     prefix=(0, 600), tail=(0, 255), num_pages=40))
