@@ -53,7 +53,9 @@ def build(verbose: bool = False) -> str:
     with ThreadPoolExecutor(min(8, len(srcs))) as ex:
         outs = list(ex.map(compile_one, zip(srcs, objs)))
     tmp = LIB + ".tmp"
-    outs.append(_run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]))
+    # rocBLAS runs the recompute pass's plain matrix products
+    outs.append(_run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-L/opt/rocm/lib", "-lrocblas",
+                      "-o", tmp]))
     os.replace(tmp, LIB)
     if verbose:
         for o in outs:

@@ -76,4 +76,22 @@ hipError_t launch_commit(const Geom& g, const int32_t* trig, int32_t* block_tabl
                          int32_t* seq_lens, const int32_t* win_start, int32_t* freed,
                          int32_t* n_freed, const int32_t* status, hipStream_t stream);
 
+// Window recompute pass (kara_attn.hip, kara_recompute_ops.hip).
+// Validation of the listed sequences for the recompute pass: index, duplicate,
+// window inside the sequence, pages of [0, p0 + W) inside the pool.
+hipError_t launch_recompute_validate(const Geom& g, const int32_t* trig, const int32_t* block_table,
+                                     const int32_t* seq_lens, const int32_t* win_start, int32_t* status,
+                                     hipStream_t stream);
+// Causal attention of q [n_trig][W][Hq][d] over one layer's cache; skips
+// sequences whose status is non-zero.
+hipError_t launch_recompute_attention(const Geom& g, const void* q, const void* k_pool, const void* v_pool,
+                                      const int32_t* trig, const int32_t* block_table, const int32_t* win_start,
+                                      void* out, const int32_t* status, hipStream_t stream);
+
+hipError_t launch_rmsnorm(const float* h, const void* gamma, void* x, int64_t n_tok, int D, float eps,
+                          hipStream_t stream);
+hipError_t launch_rope(const void* qraw, void* q_out, int n_trig, int W, int Hq, int d, float theta,
+                       const int32_t* trig, const int32_t* rope_pos0, const int32_t* status, hipStream_t stream);
+hipError_t launch_swiglu(void* gate, const void* up, int64_t n, hipStream_t stream);
+
 }  // namespace kara

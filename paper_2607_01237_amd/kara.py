@@ -14,7 +14,8 @@ import re
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libkara.so")
-HEADERS = [os.path.join(os.path.dirname(_PKG), "include", h) for h in ("kara.h", "kara_harness.h", "kara_sched.h")]
+HEADERS = [os.path.join(os.path.dirname(_PKG), "include", h)
+           for h in ("kara.h", "kara_harness.h", "kara_sched.h", "kara_recompute.h")]
 
 BF16, F32 = 0, 1
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_SCHED_MISMATCH = 0, -1, -2, -3, -4, -5
@@ -47,6 +48,15 @@ class KaraParams(ctypes.Structure):
         ("scale", ctypes.c_float),
         ("score_queries", ctypes.c_int32),
     ]
+
+
+class KaraModel(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("ffn", ctypes.c_int32), ("rope_theta", ctypes.c_float),
+                ("rms_eps", ctypes.c_float)]
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("w_q", "w_o", "w_gate", "w_up", "w_down", "g_attn", "g_ffn")]
 
 
 class SchedConfig(ctypes.Structure):
@@ -116,6 +126,11 @@ _SIGS = {
     "kara_harness_decode_workspace_size": (_I32, [_PAR, _I32, _I32, _I32, ctypes.POINTER(ctypes.c_size_t)]),
     "kara_harness_decode_attention": (_I32, [_PAR, _I32, _VP, _I32, _VP, _PP, _PP, _VP, _VP, _I32, _VP, _VP,
                                              ctypes.c_size_t, _VP]),
+    "kara_recompute_attention": (_I32, [_PAR, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
+    "kara_recompute_workspace_size": (_I32, [_PAR, ctypes.POINTER(KaraModel), _I32,
+                                             ctypes.POINTER(ctypes.c_size_t)]),
+    "kara_recompute_queries": (_I32, [_PAR, ctypes.POINTER(KaraModel), _I32, _VP, _I32, ctypes.POINTER(LayerWeights),
+                                      _VP, _VP, _PP, _PP, _VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP]),
     "kara_sched_create": (_I32, [ctypes.POINTER(SchedConfig), _P32, ctypes.POINTER(ctypes.c_void_p)]),
     "kara_sched_destroy": (_I32, [_VP]),
     "kara_sched_submit": (_I32, [_VP, _I32, _I32, _P64]),
@@ -285,6 +300,41 @@ def decode_attention(p, seqs, q, k_pools, v_pools, block_table, seq_lens, max_le
     _check("kara_harness_decode_attention", load().kara_harness_decode_attention(
         ctypes.byref(p), seqs.numel(), _ptr(seqs), len(k_pools), _ptr(q), _ptr_array(k_pools),
         _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), max_len, _ptr(out), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+# ---- window recompute pass (include/kara_recompute.h)
+
+def recompute_attention(p, trig, q, k_pool, v_pool, block_table, seq_lens, win_start, out, status, stream=None):
+    """Causal attention of q [n_trig][W][Hq][d] (bf16) over one layer's paged cache into out."""
+    _check("kara_recompute_attention", load().kara_recompute_attention(
+        ctypes.byref(p), trig.numel(), _ptr(trig), _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(block_table),
+        _ptr(seq_lens), _ptr(win_start), _ptr(out), _ptr(status), _stream(stream)))
+
+
+def make_model(hidden, ffn, rope_theta=1e6, rms_eps=1e-6) -> KaraModel:
+    return KaraModel(int(hidden), int(ffn), float(rope_theta), float(rms_eps))
+
+
+def recompute_workspace_size(p, m: KaraModel, n_trig: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check("kara_recompute_workspace_size", load().kara_recompute_workspace_size(
+        ctypes.byref(p), ctypes.byref(m), int(n_trig), ctypes.byref(out)))
+    return int(out.value)
+
+
+def recompute_queries(p, m: KaraModel, trig, weights, hidden_in, hidden_out, k_pools, v_pools, block_table,
+                      seq_lens, win_start, rope_pos0, q_out, status, workspace, stream=None):
+    """The window recompute pass over len(weights) layers; weights: one dict
+    per layer of bf16 tensors w_q, w_o, w_gate, w_up, w_down, g_attn, g_ffn."""
+    n = len(weights)
+    arr = (LayerWeights * n)()
+    for i, w in enumerate(weights):
+        arr[i] = LayerWeights(*[_ptr(w[f]).value for f, _ in LayerWeights._fields_])
+    _check("kara_recompute_queries", load().kara_recompute_queries(
+        ctypes.byref(p), ctypes.byref(m), trig.numel(), _ptr(trig), n, arr, _ptr(hidden_in), _ptr(hidden_out),
+        _ptr_array(k_pools), _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), _ptr(win_start),
+        _ptr(rope_pos0), _ptr(q_out), _ptr(status), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
 
 

@@ -1,0 +1,226 @@
+"""GPU parity of the window recompute pass (App. C.2) against the oracle.
+
+Attention (kara_recompute_attention): every output element against the
+oracle's fp64 causal attention over the same bf16 rows, within
+
+    |o_gpu - o_ora| <= 2^-8 (|o_ora| + 1)
+
+The kernel rounds the softmax weights to bf16 (relative error up to
+u = 2^-8 each, random in sign) before the value product and rounds the
+output to bf16 (u|o|); with N(0,1) values the weighted sum of the weight
+errors stays well below u, and fp32 accumulation adds far less.
+
+Whole pass (kara_recompute_queries): each layer against the oracle's layer
+fed the GPU's own fp32 residual stream entering it.  bf16 keeps 8
+significant bits, unit roundoff u = 2^-8.  The GPU stores in bf16 the
+normalised activations x (error u|x_i|, which reaches q_j through the
+product as about u rms(q)), the projected queries (u times the pair the
+rotation mixes) and the rotated queries (u|q_j|).  With pn_j the norm of
+the rotated pair holding j:
+
+    q:  |q_gpu - q_ora| <= 2u (|q_ora| + pn + 2 rms(q_ora row))
+
+The residual update dh = h_out - h_in passes through five bf16 stores
+(attention output, normalised activations, gate, up, their product) and the
+attention's own error (above).  Each store adds noise of random sign on
+the order of u times its branch's scale, so the error of dh is noise of
+about u rms(dh); its largest element over tens of thousands reaches some
+4.5 standard deviations.  Elementwise, and for the noise as a whole:
+
+    h:  |dh_gpu - dh_ora| <= 8u (|dh_ora| + rms(dh_ora row))
+        rms(dh_gpu - dh_ora) <= 2u rms(dh_ora)      (also for q)
+
+A wrong sign, index, activation or operand order gives errors of order
+rms(dh) itself, hundreds of u.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import kara_inputs as ki
+from oracle import kara_recompute as rc
+from oracle import to_f64
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _setup(n_seqs, window, n_q, n_kv, d, bs, prefix, tail=(0, 8), seed=0):
+    cfg = ki.workload("batch8", n_seqs=n_seqs, n_layers=1, window=window, buffer=0, budget=max(1, window // 5),
+                      chunk_budget=0, n_q_heads=n_q, n_kv_heads=n_kv, head_dim=d, block_size=bs, prefix=prefix,
+                      tail=tail, num_pages=None, pool_slack=0.25, seed=seed)
+    geom = ki.make_geometry(cfg)
+    p = geom.params()
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed + 100)
+    shape = (geom.num_pages, n_kv, bs, d)
+    kp = torch.randn(shape, generator=g, device=dev).to(torch.bfloat16)
+    vp = torch.randn(shape, generator=g, device=dev).to(torch.bfloat16)
+    nt = len(geom.trig)
+    q = torch.randn((nt, window, n_q, d), generator=g, device=dev).to(torch.bfloat16)
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    return geom, p, q, kp, vp, T(geom.trig), T(geom.block_table), T(geom.seq_lens), T(geom.win_start)
+
+
+def _oracle_attention(geom, p, q_h, kp_h, vp_h, t, rows=None):
+    s = int(geom.trig[t])
+    p0 = int(geom.win_start[s])
+    W = p["window"]
+    to64 = lambda a: to_f64(a, "bf16")
+    kr = rc.cache_rows(kp_h, geom.block_table[s], p0 + W, p["block_size"], to64)
+    vr = rc.cache_rows(vp_h, geom.block_table[s], p0 + W, p["block_size"], to64)
+    qs = to64(q_h[t])
+    return rc.causal_window_attention(qs, kr, vr, p0, 1.0 / math.sqrt(p["head_dim"]))
+
+
+@pytest.mark.parametrize("window,n_q,n_kv,d,bs,prefix", [
+    (64, 8, 2, 128, 16, (0, 0)),           # no prefix: token 0 sees only itself
+    (200, 8, 2, 128, 16, (0, 300)),        # window not a multiple of a chunk, ragged prefix
+    (96, 40, 8, 128, 7, (10, 130)),        # G = 5 (Qwen3-14B), unaligned blocks
+    (128, 4, 4, 64, 16, (0, 100)),         # G = 1, d = 64
+    (256, 32, 8, 128, 256, (0, 600)),      # serving geometry: 256-token blocks
+])
+def test_attention_parity(window, n_q, n_kv, d, bs, prefix):
+    from paper_2607_01237_amd import kara
+    _need_gpu()
+    print(f"\n[case] recompute attention W={window} {n_q}/{n_kv} d={d} bs={bs} prefix={prefix}", flush=True)
+    geom, p, q, kp, vp, trig, bt, lens, ws = _setup(3, window, n_q, n_kv, d, bs, prefix)
+    params = kara.make_params(p, geom.block_table.shape[0])
+    out = torch.full_like(q, float("nan"))
+    status = torch.full((len(geom.trig),), -7, dtype=torch.int32, device=q.device)
+    kara.recompute_attention(params, trig, q, kp, vp, bt, lens, ws, out, status)
+    torch.cuda.synchronize()
+    assert (status.cpu().numpy() == 0).all()
+    got = to_f64(ki.raw_numpy(out), "bf16")
+    q_h, kp_h, vp_h = ki.raw_numpy(q), ki.raw_numpy(kp), ki.raw_numpy(vp)
+    worst = 0.0
+    for t in range(len(geom.trig)):
+        want = _oracle_attention(geom, p, q_h, kp_h, vp_h, t)
+        err = np.abs(got[t] - want)
+        tol = 2.0 ** -8 * (np.abs(want) + 1.0)
+        bad = err > tol
+        assert not bad.any(), f"trigger {t}: {bad.sum()} elements out of tolerance, max err {err.max():.3e}"
+        worst = max(worst, float(err.max()))
+    print(f"[case] ok, max abs err {worst:.2e}", flush=True)
+
+
+def test_attention_flags_bad_windows():
+    from paper_2607_01237_amd import kara
+    _need_gpu()
+    print("\n[case] recompute attention status flags", flush=True)
+    geom, p, q, kp, vp, trig, bt, lens, ws = _setup(3, 64, 8, 2, 128, 16, (0, 50))
+    params = kara.make_params(p, geom.block_table.shape[0])
+    bad_ws = ws.clone()
+    s1 = int(geom.trig[1])
+    bad_ws[s1] = int(geom.seq_lens[s1]) - 10          # window runs past the end
+    trig2 = trig.clone()
+    trig2[2] = trig2[0]                                # listed twice
+    out = torch.zeros_like(q)
+    status = torch.full((len(geom.trig),), -7, dtype=torch.int32, device=q.device)
+    kara.recompute_attention(params, trig2, q, kp, vp, bt, lens, bad_ws, out, status)
+    torch.cuda.synchronize()
+    st = status.cpu().numpy()
+    assert st[1] == kara.SEQ_BAD_WINDOW
+    assert st[0] & kara.SEQ_DUP_TRIGGER and st[2] & kara.SEQ_DUP_TRIGGER
+    assert (out[1].float() == 0).all() and (out[2].float() == 0).all()
+
+
+def _weights(rng_t, L, D, F, HD, dev):
+    def w(shape, fan_in):
+        return (torch.randn(shape, generator=rng_t, device=dev) / math.sqrt(fan_in)).to(torch.bfloat16)
+    out = []
+    for _ in range(L):
+        out.append(dict(w_q=w((D, HD), D), w_o=w((HD, D), HD), w_gate=w((D, F), D), w_up=w((D, F), D),
+                        w_down=w((F, D), F),
+                        g_attn=(1.0 + 0.1 * torch.randn(D, generator=rng_t, device=dev)).to(torch.bfloat16),
+                        g_ffn=(1.0 + 0.1 * torch.randn(D, generator=rng_t, device=dev)).to(torch.bfloat16)))
+    return out
+
+
+def _f64(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+@pytest.mark.parametrize("window,n_q,n_kv,d,D,F,bs", [
+    (64, 8, 2, 128, 512, 1024, 16),
+    (80, 10, 2, 64, 384, 768, 7),
+])
+def test_recompute_pass_layers(window, n_q, n_kv, d, D, F, bs):
+    from paper_2607_01237_amd import kara
+    _need_gpu()
+    L = 2
+    print(f"\n[case] recompute pass W={window} {n_q}/{n_kv} d={d} D={D} F={F} bs={bs}", flush=True)
+    geom, p, _, kp0, vp0, trig, bt, lens, ws = _setup(3, window, n_q, n_kv, d, bs, (0, 200), seed=1)
+    dev = kp0.device
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    kp = [kp0] + [torch.randn_like(kp0, dtype=torch.float32).to(torch.bfloat16) for _ in range(L - 1)]
+    vp = [vp0] + [torch.randn_like(vp0, dtype=torch.float32).to(torch.bfloat16) for _ in range(L - 1)]
+    wts = _weights(g, L, D, F, n_q * d, dev)
+    nt = len(geom.trig)
+    h0 = torch.randn((nt, window, D), generator=g, device=dev)
+    rope_pos0 = (torch.from_numpy(geom.win_start).to(dev) + 5000).to(torch.int32)   # positions after compressions
+    params = kara.make_params(p, geom.block_table.shape[0])
+    model = kara.make_model(D, F, rope_theta=1e6, rms_eps=1e-6)
+    wsp = torch.empty(kara.recompute_workspace_size(params, model, nt), dtype=torch.uint8, device=dev)
+    status = torch.full((nt,), -7, dtype=torch.int32, device=dev)
+
+    # layer by layer, each from the GPU's own residual stream
+    h = h0.clone()
+    q_layers = []
+    for l in range(L):
+        h_next = torch.empty_like(h)
+        q = torch.empty((1, nt, window, n_q, d), dtype=torch.bfloat16, device=dev)
+        kara.recompute_queries(params, model, trig, [wts[l]], h, h_next, [kp[l]], [vp[l]], bt, lens, ws, rope_pos0,
+                               q, status, wsp)
+        torch.cuda.synchronize()
+        assert (status.cpu().numpy() == 0).all()
+        wt64 = {k_: _f64(v_) for k_, v_ in wts[l].items()}
+        dims = dict(n_q_heads=n_q, head_dim=d, rms_eps=1e-6, rope_theta=1e6, block_size=bs)
+        to64 = lambda a: to_f64(a, "bf16")
+        kh, vh = ki.raw_numpy(kp[l]), ki.raw_numpy(vp[l])
+        for t in range(nt):
+            s = int(geom.trig[t])
+            p0 = int(geom.win_start[s])
+            kr = rc.cache_rows(kh, geom.block_table[s], p0 + window, bs, to64)
+            vr = rc.cache_rows(vh, geom.block_table[s], p0 + window, bs, to64)
+            hin = _f64(h[t])
+            q_ora, h_ora, _ = rc.recompute_layer(hin, wt64, kr, vr, p0, p0 + 5000, dims)
+            q_gpu = to_f64(ki.raw_numpy(q[0, t]), "bf16")
+            rms = np.sqrt((q_ora ** 2).mean(axis=-1, keepdims=True))
+            half = d // 2
+            pn = np.sqrt(q_ora[..., :half] ** 2 + q_ora[..., half:] ** 2)
+            pn = np.concatenate([pn, pn], axis=-1)
+            err = np.abs(q_gpu - q_ora)
+            ratio_q = float((err / (np.abs(q_ora) + pn + 2 * rms)).max()) / 2.0 ** -8
+            dh_ora = h_ora - hin
+            dh_gpu = _f64(h_next[t]) - hin
+            rms_h = np.sqrt((dh_ora ** 2).mean(axis=-1, keepdims=True))
+            err_h = np.abs(dh_gpu - dh_ora)
+            ratio_h = float((err_h / (np.abs(dh_ora) + rms_h)).max()) / 2.0 ** -8
+            noise_q = float(np.sqrt((err ** 2).mean() / (q_ora ** 2).mean())) / 2.0 ** -8
+            noise_h = float(np.sqrt((err_h ** 2).mean() / (dh_ora ** 2).mean())) / 2.0 ** -8
+            print(f"[case] layer {l} trigger {t}: q err {err.max():.3e} ({ratio_q:.2f} of 2 u), noise {noise_q:.2f} u; "
+                  f"dh err {err_h.max():.3e} ({ratio_h:.2f} of 8 u), noise {noise_h:.2f} u", flush=True)
+            assert ratio_q <= 2.0, f"layer {l} trigger {t}: q max err {err.max():.3e}"
+            assert ratio_h <= 8.0, f"layer {l} trigger {t}: h max err {err_h.max():.3e}"
+            assert noise_q <= 2.0 and noise_h <= 2.0, (noise_q, noise_h)
+        q_layers.append(q[0].clone())
+        h = h_next
+
+    # one call over both layers gives the same bits as the layer-by-layer calls
+    q_all = torch.empty((L, nt, window, n_q, d), dtype=torch.bfloat16, device=dev)
+    h_all = torch.empty_like(h0)
+    kara.recompute_queries(params, model, trig, wts, h0, h_all, kp, vp, bt, lens, ws, rope_pos0, q_all, status, wsp)
+    torch.cuda.synchronize()
+    for l in range(L):
+        assert torch.equal(q_all[l].view(torch.int16), q_layers[l].view(torch.int16)), f"layer {l} queries"
+    assert torch.equal(h_all, h)
+    print("[case] ok", flush=True)
