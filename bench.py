@@ -19,6 +19,7 @@ sample of units on this host.
     python bench.py [--steps K] [--warmup W] [--workload qwen14b|batch8|ragged|buffer_only|threshold_topk|prefill]
     python bench.py --workload soak [--intervals n] [--warmup W]
     python bench.py --workload serve [--requests n]
+    python bench.py --workload recompute [--steps K] [--warmup W]
 
 The soak runs the compression step inside a decode loop (append, decode
 attention, compress, reclaim pages; paper_2607_01237_amd/soak.py) and reports
@@ -400,6 +401,126 @@ def run_soak(args):
     print(json.dumps(result), flush=True)
 
 
+def run_recompute(args):
+    """A compression event with its query recomputation (App. C.2): the
+    window recompute pass over every layer (query projection, rotary
+    embedding, causal attention over the cached prefix, feed-forward) writes
+    the scoring queries, then kara_compress_window compresses every window
+    with them.  Synthetic weights of the named shape.  Reports window tokens
+    per second of the whole event, the recompute's share, and the roofline of
+    the attention kernel (timed one layer per launch through
+    kara_recompute_attention, HIP events on the launch stream)."""
+    import torch
+
+    import kara_inputs as ki
+    from paper_2607_01237_amd import kara
+
+    kara.load()
+    device = torch.device("cuda:0")
+    torch.cuda.set_device(device)
+    cfg = ki.workload("recompute")
+    geom, p, params, q_unused, kp, vp, meta = setup(cfg, device)
+    del q_unused
+    L, nt, H = cfg["n_layers"], len(geom.trig), p["n_kv_heads"]
+    W, N, d, Hq = p["window"], p["window"] - p["buffer"], p["head_dim"], p["n_q_heads"]
+    D, F = cfg["hidden"], cfg["ffn"]
+    G = Hq // H
+    gen = torch.Generator(device=device)
+    gen.manual_seed(cfg["seed"] + 1)
+
+    def w(shape, fan_in):
+        return (torch.randn(shape, generator=gen, device=device) / fan_in ** 0.5).to(torch.bfloat16)
+
+    wts = [dict(w_q=w((D, Hq * d), D), w_o=w((Hq * d, D), Hq * d), w_gate=w((D, F), D), w_up=w((D, F), D),
+                w_down=w((F, D), F), g_attn=torch.ones(D, dtype=torch.bfloat16, device=device),
+                g_ffn=torch.ones(D, dtype=torch.bfloat16, device=device)) for _ in range(L)]
+    model = kara.make_model(D, F, cfg["rope_theta"], cfg["rms_eps"])
+    h0 = torch.randn((nt, W, D), generator=gen, device=device)
+    h1 = torch.empty_like(h0)
+    q = torch.empty((L, nt, W, Hq, d), dtype=torch.bfloat16, device=device)
+    rope_pos0 = meta["win_start"].clone()
+    rws = torch.empty(kara.recompute_workspace_size(params, model, nt), dtype=torch.uint8, device=device)
+    cws = torch.empty(kara.workspace_size(params, nt, L), dtype=torch.uint8, device=device)
+    status = torch.empty(nt, dtype=torch.int32, device=device)
+    rstatus = torch.empty(nt, dtype=torch.int32, device=device)
+    freed = torch.empty((nt, p["max_blocks_per_seq"]), dtype=torch.int32, device=device)
+    n_freed = torch.empty(nt, dtype=torch.int32, device=device)
+    stream = torch.cuda.current_stream()
+    log(f"recompute: {nt} sequences x {L} layers, D={D} F={F}, mem {torch.cuda.memory_allocated() / 2**30:.1f} GiB")
+
+    def restore():
+        meta["bt"].copy_(meta["bt0"], non_blocking=True)
+        meta["seq_lens"].copy_(meta["seq_lens0"], non_blocking=True)
+
+    def event(evs=None):
+        restore()
+        if evs:
+            evs[0].record(stream)
+        kara.recompute_queries(params, model, meta["trig"], wts, h0, h1, kp, vp, meta["bt"], meta["seq_lens"],
+                               meta["win_start"], rope_pos0, q, rstatus, rws, stream=stream)
+        if evs:
+            evs[1].record(stream)
+        kara.compress_window(params, meta["trig"], q, kp, vp, meta["bt"], meta["seq_lens"], meta["win_start"], True,
+                             status, cws, freed=freed, n_freed=n_freed, stream=stream)
+        if evs:
+            evs[2].record(stream)
+
+    for _ in range(args.warmup):
+        event()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        event(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    assert (rstatus.cpu().numpy() == 0).all() and (status.cpu().numpy() == 0).all()
+    rec_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in evs]))
+    comp_ms = float(np.mean([b.elapsed_time(c) for _, b, c in evs]))
+    ms = wall * 1e3 / args.steps
+
+    # the attention kernel alone, one layer per launch
+    restore()
+    att_out = torch.empty((nt, W, Hq, d), dtype=torch.bfloat16, device=device)
+    att_ms = []
+    for rep in range(2):
+        for l in range(L):
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            e[0].record(stream)
+            kara.recompute_attention(params, meta["trig"], q[l], kp[l], vp[l], meta["bt"], meta["seq_lens"],
+                                     meta["win_start"], att_out, rstatus, stream=stream)
+            e[1].record(stream)
+            torch.cuda.synchronize()
+            if rep:
+                att_ms.append(e[0].elapsed_time(e[1]))
+    att_ms = float(np.mean(att_ms))
+    p0 = geom.win_start[geom.trig].astype(np.float64)
+    # QK^T and PV over the causal extent: query w sees p0 + w + 1 keys
+    att_flops = float(sum(4.0 * G * H * d * (W * (p0_ + 1) + W * (W - 1) / 2) for p0_ in p0))
+    att_ach = att_flops / (att_ms * 1e-3) / 1e12
+    gemm_flops = 2.0 * nt * W * (2 * D * Hq * d + 3 * D * F) * L
+    win_tokens = nt * W
+    result = {
+        "metric": "window tokens compressed/s, compression event with query recomputation",
+        "value": win_tokens / (ms * 1e-3),
+        "unit": "window tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) hidden states, K/V and weights of the named shape; no checkpoint)",
+        "config": {"workload": "recompute", "sequences": nt, "layers": L, "q_heads": Hq, "kv_heads": H,
+                   "head_dim": d, "hidden": D, "ffn": F, "window": W, "budget": p["budget"],
+                   "context_tokens_mean": float(geom.seq_lens[geom.trig].mean())},
+        "roofline": {"kernel": "attn_kernel (recompute causal attention)", "bound": "mfma", "achieved": att_ach,
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": att_ach / PEAK_BF16_TFLOPS,
+                     "traffic": None, "flop_per_launch": att_flops, "avg_launch_ms": att_ms},
+        "recompute": {"recompute_ms": rec_ms, "compress_ms": comp_ms, "attention_ms_total": att_ms * L,
+                      "attention_tflop_total": att_flops * L / 1e12, "gemm_tflop_total": gemm_flops / 1e12,
+                      "rest_ms": rec_ms - att_ms * L,
+                      "gemm_and_rest_tflops": gemm_flops / ((rec_ms - att_ms * L) * 1e-3) / 1e12},
+    }
+    print(json.dumps(result), flush=True)
+
+
 def run_serve(args):
     """The serving analogue of the paper's throughput runs (App. B.1): a batch
     of requests served to completion by the periodic policy on a memory-bound
@@ -488,6 +609,9 @@ def main():
         return
     if args.workload == "serve":
         run_serve(args)
+        return
+    if args.workload == "recompute":
+        run_recompute(args)
         return
     import torch
 

@@ -86,6 +86,11 @@ BASE = {
                     window=1024, buffer=0, budget=205, max_chunk_len=8, chunk_budget=16,
                     block_size=16, num_pages=None, seed=7, prefix=(0, 0), tail=(0, 1023),
                     pool_slack=0.10, key_mode="normal", n_windows=16),
+    "recompute": dict(n_seqs=16, n_layers=36, n_q_heads=32, n_kv_heads=8, head_dim=128, dtype="bf16",
+                      window=1024, buffer=0, budget=205, max_chunk_len=8, chunk_budget=16,
+                      block_size=16, num_pages=None, seed=9, prefix=(3072, 15360), tail=(0, 15),
+                      pool_slack=0.05, key_mode="normal", hidden=4096, ffn=12288, rope_theta=1e6,
+                      rms_eps=1e-6),
     "soak": dict(n_seqs=128, n_layers=40, n_q_heads=40, n_kv_heads=8, head_dim=128, dtype="bf16",
                  window=1024, buffer=0, budget=205, max_chunk_len=8, chunk_budget=16,
                  block_size=16, num_pages=None, seed=4, prefix=(1024, 1024), tail=(0, 0),

@@ -37,18 +37,16 @@ template <int D, int QT>
 struct ACfg {
   static constexpr int kRowBytes = D * 2;
   static constexpr int kCPR = kRowBytes / 16;          // 16-byte chunks per row
+  static constexpr int kSwz = kCPR - 1;                // XOR swizzle of chunks by row
   static constexpr int kKS = kCPR / 4;                 // k-steps of one dot product (per lane group)
   static constexpr int kDT = D / 16;                   // 16-row tiles of O^T
   static constexpr int kRowsWave = 16 * QT;
   static constexpr int kRowsWG = kAttnWaves * kRowsWave;
-  static constexpr int kKBytes = kKeys * kRowBytes;    // one K chunk
-  static constexpr int kVRow = kKeys * 2;              // one V^T row (d fixed): 128 bytes
-  static constexpr int kVBytes = D * kVRow;
-  static constexpr int kStage = kKBytes + kVBytes;
-  static constexpr int kKLoads = kKeys * kCPR / kAttnThreads;        // 16-byte K loads per thread
-  static constexpr int kVItems = (kKeys / 4) * kCPR;                 // (4-key unit, d chunk) items
-  static_assert(kKLoads * kAttnThreads == kKeys * kCPR, "uniform K loads");
-  static_assert(kVItems <= kAttnThreads, "one V item per thread at most");
+  static constexpr int kKBytes = kKeys * kRowBytes;    // one chunk of K (or V) rows
+  static constexpr int kStage = 2 * kKBytes;           // K rows, then V rows
+  static constexpr int kStages = 2;
+  static constexpr int kCopies = kKBytes / (kAttnThreads * 16);      // 16-byte copies per thread per pool
+  static_assert(kCopies * kAttnThreads * 16 == kKBytes, "uniform copies");
 };
 
 struct AttnArgs {
@@ -73,10 +71,44 @@ __device__ inline float wave_max4(float v) {
   return v;
 }
 
+// Direct global->LDS copy of 16 bytes per lane; lane i's bytes land at
+// lds_wave_base + 16*i (global_load_lds_dwordx4, LDS base in M0).  Issued
+// through inline assembly so the compiler adds no wait of its own before
+// LDS reads; the kernel waits explicitly.  M0 is restored.
+__device__ inline void copy16(const void* g, char* lds_wave_base) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds_wave_base);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(g), "s"(lds)
+      : "memory");
+}
+
+// Barrier for LDS traffic only (the copies it covers are waited for first).
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+__device__ inline void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+
+// Transposed LDS read (gfx950): within each 16-lane group, lane 4j+e gets
+// element e of the 4-element rows addressed by lanes j, j+4, j+8, j+12.
+__device__ inline v4i16 read_tr(const char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4i16*)(__attribute__((address_space(3))) char*)p);
+}
+
 template <int D, int QT>
 __global__ __launch_bounds__(kAttnThreads) void attn_kernel(AttnArgs a) {
   using C = ACfg<D, QT>;
-  __shared__ __attribute__((aligned(16))) char smem[2 * C::kStage];
+  __shared__ __attribute__((aligned(16))) char smem[C::kStages * C::kStage];
+  // 16-byte-unit offsets of a chunk's 64 cache rows inside a pool (K and V
+  // pools share the layout); three chunks: issuing, next, being filled
+  __shared__ uint32_t row_off[3][kKeys];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -99,7 +131,6 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(AttnArgs a) {
   const int kend = p0 + last_row / a.G + 1;           // keys this workgroup needs
   const int n_chunks = (kend + kKeys - 1) / kKeys;
   const int32_t* row_pages = a.bt + (int64_t)s * a.max_blocks;
-  const int64_t head_stride = (int64_t)a.bs * C::kRowBytes;
 
   // ---- this wave's queries as B operands (lane: query li of each tile) ----
   const int wrow0 = row0 + wave * C::kRowsWave;
@@ -115,6 +146,13 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int ks = 0; ks < C::kKS; ++ks) qop[qt][ks] = *(const uint4*)(qrow + (gq * C::kKS + ks) * 16);
   }
+  // consume the query loads before any copy is issued, so the compiler
+  // waits for them here and not inside the chunk loop
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+    for (int ks = 0; ks < C::kKS; ++ks)
+      asm volatile("" ::"v"(qop[qt][ks].x), "v"(qop[qt][ks].y), "v"(qop[qt][ks].z), "v"(qop[qt][ks].w));
   const int wave_first_pos = p0 + min(wrow0, R - 1) / a.G;
   const int wave_last_pos = p0 + min(wrow0 + C::kRowsWave - 1, R - 1) / a.G;
 
@@ -128,65 +166,53 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(AttnArgs a) {
     for (int dt = 0; dt < C::kDT; ++dt) o[qt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // ---- staging of one chunk: global -> registers -> LDS ----
-  uint4 kst[C::kKLoads];
-  uint4 vst[4];
-  const bool v_item = tid < C::kVItems;
-  const int v_unit = tid / C::kCPR;       // keys 4*v_unit .. +3
-  const int v_chunk = tid % C::kCPR;      // d 8*v_chunk .. +7
-  auto row_ptr = [&](const char* pool, int pos) -> const char* {
-    const int64_t page = row_pages[pos / a.bs];
-    return pool + (page * a.Hkv + h) * head_stride + (int64_t)(pos % a.bs) * C::kRowBytes;
+  // ---- row offsets (wave 0, one lane per row) and copies ----
+  // rows past kend repeat row kend - 1: finite, and masked for every query
+  auto page_of = [&](int ch) -> int {
+    const int pos = min(ch * kKeys + lane, kend - 1);
+    return row_pages[pos / a.bs];
   };
-  auto load_chunk = [&](int k0) __attribute__((always_inline)) {
-#pragma unroll
-    for (int j = 0; j < C::kKLoads; ++j) {
-      const int idx = j * kAttnThreads + tid;
-      const int key = idx / C::kCPR, c = idx % C::kCPR;
-      const int pos = k0 + key;
-      kst[j] = pos < kend ? *(const uint4*)(row_ptr(a.kpool, pos) + c * 16) : uint4{0, 0, 0, 0};
-    }
-    if (v_item) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int pos = k0 + 4 * v_unit + i;
-        vst[i] = pos < kend ? *(const uint4*)(row_ptr(a.vpool, pos) + v_chunk * 16) : uint4{0, 0, 0, 0};
-      }
-    }
+  auto put_offset = [&](int ch, int page) {
+    const int pos = min(ch * kKeys + lane, kend - 1);
+    row_off[ch % 3][lane] = (uint32_t)((((int64_t)page * a.Hkv + h) * a.bs + pos % a.bs) * C::kCPR);
   };
-  auto store_chunk = [&](char* st) __attribute__((always_inline)) {
+  // copy r of this thread fills slot r*256 + tid of the K (V) region: row
+  // kr = slot / kCPR, stored chunk slot % kCPR, fetched chunk (slot % kCPR) ^ (kr & kSwz)
+  int kr_of[C::kCopies], chunk_of[C::kCopies];
 #pragma unroll
-    for (int j = 0; j < C::kKLoads; ++j) {
-      const int idx = j * kAttnThreads + tid;
-      const int key = idx / C::kCPR, c = idx % C::kCPR;
-      *(uint4*)(st + key * C::kRowBytes + ((c ^ (key & (C::kCPR - 1))) * 16)) = kst[j];
-    }
-    if (v_item) {
-      char* vt = st + C::kKBytes;
-      const uint16_t* e0 = (const uint16_t*)&vst[0];
-      const uint16_t* e1 = (const uint16_t*)&vst[1];
-      const uint16_t* e2 = (const uint16_t*)&vst[2];
-      const uint16_t* e3 = (const uint16_t*)&vst[3];
+  for (int r = 0; r < C::kCopies; ++r) {
+    const int slot = r * kAttnThreads + tid;
+    kr_of[r] = slot / C::kCPR;
+    chunk_of[r] = (slot % C::kCPR) ^ (kr_of[r] & C::kSwz);
+  }
+  auto issue = [&](int ch) __attribute__((always_inline)) {
+    char* st = smem + (ch % C::kStages) * C::kStage;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int d = v_chunk * 8 + e;
-        uint2 packed;
-        packed.x = (uint32_t)e0[e] | ((uint32_t)e1[e] << 16);
-        packed.y = (uint32_t)e2[e] | ((uint32_t)e3[e] << 16);
-        *(uint2*)(vt + d * C::kVRow + ((v_unit ^ (d & 15)) * 8)) = packed;
-      }
+    for (int r = 0; r < C::kCopies; ++r) {
+      const uint64_t off = (uint64_t)row_off[ch % 3][kr_of[r]] * 16 + chunk_of[r] * 16;
+      copy16(a.kpool + off, st + (r * kAttnWaves + wave) * 1024);
+      copy16(a.vpool + off, st + C::kKBytes + (r * kAttnWaves + wave) * 1024);
     }
   };
 
-  load_chunk(0);
-  store_chunk(smem);
-  __syncthreads();
+  if (wave == 0) {
+    put_offset(0, page_of(0));
+    if (n_chunks > 1) put_offset(1, page_of(1));
+  }
+  lds_barrier();
+  issue(0);
 
+  // per-lane LDS byte offsets of the operand reads (rows are 16*tile + li
+  // for K, 32*j + 16*half + 4*gq + (li >> 2) for V, so the swizzle term
+  // depends on the lane and the compile-time indices only)
   for (int ch = 0; ch < n_chunks; ++ch) {
+    wait_copies();
+    lds_barrier();
+    if (ch + 1 < n_chunks) issue(ch + 1);
+    int next_page = 0;
+    if (wave == 0 && ch + 2 < n_chunks) next_page = page_of(ch + 2);
     const int k0 = ch * kKeys;
-    const bool more = ch + 1 < n_chunks;
-    if (more) load_chunk(k0 + kKeys);
-    const char* st = smem + (ch & 1) * C::kStage;
+    const char* st = smem + (ch % C::kStages) * C::kStage;
     if (k0 <= wave_last_pos) {
       const bool diag = k0 + kKeys - 1 > wave_first_pos;
       // S^T tiles: keys kt*16 + (4*gq + r), query li
@@ -202,7 +228,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(AttnArgs a) {
         for (int ks = 0; ks < C::kKS; ++ks) {
           const int c = gq * C::kKS + ks;
           bf16x8 ka;
-          __builtin_memcpy(&ka, st + key * C::kRowBytes + ((c ^ (key & (C::kCPR - 1))) * 16), 16);
+          __builtin_memcpy(&ka, st + key * C::kRowBytes + ((c ^ (key & C::kSwz)) * 16), 16);
 #pragma unroll
           for (int qt = 0; qt < QT; ++qt) {
             bf16x8 qb;
@@ -211,22 +237,19 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(AttnArgs a) {
           }
         }
       }
-      // online softmax per query (lane's query li of each tile)
+      // online softmax per query (lane's query li of each tile), in log2 units
       bf16x8 pb[QT][2];
 #pragma unroll
       for (int qt = 0; qt < QT; ++qt) {
-        float x[4][4];
         float cmax = kNegInf;
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            float v = sv[qt][kt][r] * a.c;
-            if (diag && k0 + kt * 16 + 4 * gq + r > qpos[qt]) v = kNegInf;
-            x[kt][r] = v;
-            cmax = fmaxf(cmax, v);
+            if (diag && k0 + kt * 16 + 4 * gq + r > qpos[qt]) sv[qt][kt][r] = kNegInf;
+            cmax = fmaxf(cmax, sv[qt][kt][r]);
           }
-        cmax = wave_max4(cmax);
+        cmax = wave_max4(cmax) * a.c;
         const float mn = fmaxf(m[qt], cmax);
         const float alpha = exp2f(m[qt] - mn);
         m[qt] = mn;
@@ -235,7 +258,7 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(AttnArgs a) {
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const float p = exp2f(x[kt][r] - mn);
+            const float p = exp2f(fmaf(sv[qt][kt][r], a.c, -mn));
             lsum += p;
             pb[qt][kt >> 1][(kt & 1) * 4 + r] = (__bf16)p;
           }
@@ -243,28 +266,30 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int dt = 0; dt < C::kDT; ++dt) o[qt][dt] *= alpha;
       }
-      // O^T += V^T P^T, two 32-key halves
-      const char* vt = st + C::kKBytes;
+      // O^T += V^T P^T over two 32-key halves; lane (gq, li) reads, through
+      // the transposed load, keys 32j + 4gq + (li >> 2) (+16) at head-dim
+      // columns dt*16 + 4*(li & 3) .. +3 and receives four keys at column
+      // dt*16 + li
+      const char* vs = st + C::kKBytes;
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        const int u1 = 8 * j + gq, u2 = 8 * j + 4 + gq;
 #pragma unroll
         for (int dt = 0; dt < C::kDT; ++dt) {
-          const int d = dt * 16 + li;
-          const char* vrow = vt + d * C::kVRow;
-          uint2 lo = *(const uint2*)(vrow + ((u1 ^ (d & 15)) * 8));
-          uint2 hi = *(const uint2*)(vrow + ((u2 ^ (d & 15)) * 8));
-          uint4 both{lo.x, lo.y, hi.x, hi.y};
+          const int c = dt * 2 + ((li & 3) >> 1);
+          const int key1 = 32 * j + 4 * gq + (li >> 2);
+          const int key2 = key1 + 16;
+          const v4i16 lo = read_tr(vs + key1 * C::kRowBytes + ((c ^ (key1 & C::kSwz)) * 16) + (li & 1) * 8);
+          const v4i16 hi = read_tr(vs + key2 * C::kRowBytes + ((c ^ (key2 & C::kSwz)) * 16) + (li & 1) * 8);
           bf16x8 va;
-          __builtin_memcpy(&va, &both, 16);
+          __builtin_memcpy(&va, &lo, 8);
+          __builtin_memcpy((char*)&va + 8, &hi, 8);
 #pragma unroll
           for (int qt = 0; qt < QT; ++qt)
             o[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[qt][j], o[qt][dt], 0, 0, 0);
         }
       }
     }
-    if (more) store_chunk(smem + ((ch + 1) & 1) * C::kStage);
-    __syncthreads();
+    if (wave == 0 && ch + 2 < n_chunks) put_offset(ch + 2, next_page);
   }
 
   // ---- normalise and store: lane holds O^T[dt*16 + 4*gq + r][query li] ----
