@@ -15,7 +15,9 @@
 // chunk, and the probabilities, converted to bf16, are already the B
 // operand of O^T += V^T P^T (the k index of that product runs over keys in
 // the order the S^T tiles left them; V^T is read in the same order).  The
-// row sums stay per lane until the end.
+// row sums stay per lane until the end.  The softmax reference maximum is
+// raised lazily (only past a headroom of 2^8), which skips the rescaling of
+// the accumulators on almost every chunk.
 #include "kara_internal.h"
 #include "kara_recompute.h"
 
@@ -32,6 +34,7 @@ constexpr int kKeys = 64;                   // keys per chunk
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kMaxFloor = -1e30f;         // finite start of a running maximum
+constexpr float kHeadroom = 8.f;            // log2 units a row may exceed its reference maximum
 
 template <int D, int QT>
 struct ACfg {
@@ -103,7 +106,7 @@ __device__ inline v4i16 read_tr(const char* p) {
 }
 
 template <int D, int QT>
-__global__ __launch_bounds__(kAttnThreads) void attn_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(AttnArgs a) {
   using C = ACfg<D, QT>;
   __shared__ __attribute__((aligned(16))) char smem[C::kStages * C::kStage];
   // 16-byte-unit offsets of a chunk's 64 cache rows inside a pool (K and V
@@ -250,21 +253,28 @@ __global__ __launch_bounds__(kAttnThreads) void attn_kernel(AttnArgs a) {
             cmax = fmaxf(cmax, sv[qt][kt][r]);
           }
         cmax = wave_max4(cmax) * a.c;
-        const float mn = fmaxf(m[qt], cmax);
-        const float alpha = exp2f(m[qt] - mn);
-        m[qt] = mn;
+        // the reference m is raised only when some row's maximum passes it
+        // by more than kHeadroom; otherwise weights up to 2^kHeadroom are
+        // accumulated as they are (the decision is per wave)
+        if (__ballot(cmax > m[qt] + kHeadroom) != 0ull) {
+          const float mn = fmaxf(m[qt], cmax);
+          const float alpha = exp2f(m[qt] - mn);
+          m[qt] = mn;
+          l[qt] *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < C::kDT; ++dt) o[qt][dt] *= alpha;
+        }
+        const float mr = m[qt];
         float lsum = 0.f;
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const float p = exp2f(fmaf(sv[qt][kt][r], a.c, -mn));
+            const float p = exp2f(fmaf(sv[qt][kt][r], a.c, -mr));
             lsum += p;
             pb[qt][kt >> 1][(kt & 1) * 4 + r] = (__bf16)p;
           }
-        l[qt] = l[qt] * alpha + lsum;
-#pragma unroll
-        for (int dt = 0; dt < C::kDT; ++dt) o[qt][dt] *= alpha;
+        l[qt] += lsum;
       }
       // O^T += V^T P^T over two 32-key halves; lane (gq, li) reads, through
       // the transposed load, keys 32j + 4gq + (li >> 2) (+16) at head-dim
