@@ -17,7 +17,11 @@
 // the order the S^T tiles left them; V^T is read in the same order).  The
 // row sums stay per lane until the end.  The softmax reference maximum is
 // raised lazily (only past a headroom of 2^8), which skips the rescaling of
-// the accumulators on almost every chunk.
+// the accumulators on almost every chunk.  Exponentials are the bare
+// v_exp_f32: arguments below the normal range flush to 0, which is the
+// right weight there.
+#include <type_traits>
+
 #include "kara_internal.h"
 #include "kara_recompute.h"
 
@@ -205,40 +209,53 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(AttnArgs a) {
   lds_barrier();
   issue(0);
 
-  // per-lane LDS byte offsets of the operand reads (rows are 16*tile + li
-  // for K, 32*j + 16*half + 4*gq + (li >> 2) for V, so the swizzle term
-  // depends on the lane and the compile-time indices only)
-  for (int ch = 0; ch < n_chunks; ++ch) {
-    wait_copies();
-    lds_barrier();
-    if (ch + 1 < n_chunks) issue(ch + 1);
-    int next_page = 0;
-    if (wave == 0 && ch + 2 < n_chunks) next_page = page_of(ch + 2);
-    const int k0 = ch * kKeys;
-    const char* st = smem + (ch % C::kStages) * C::kStage;
-    if (k0 <= wave_last_pos) {
-      const bool diag = k0 + kKeys - 1 > wave_first_pos;
+  // Per-lane LDS byte offsets of the operand reads.  K operand rows are
+  // 16*kt + li, so row & kSwz = li & kSwz and the swizzled chunk depends on
+  // the lane and ks only; V rows read through the transposed load are
+  // 32*j + 16*half + 4*gq + (li >> 2), whose low four bits do not depend on
+  // j or half.  The tile and half offsets are then compile-time constants.
+  int koff[C::kKS], voff[C::kDT];
+#pragma unroll
+  for (int ks = 0; ks < C::kKS; ++ks)
+    koff[ks] = li * C::kRowBytes + (((gq * C::kKS + ks) ^ (li & C::kSwz)) * 16);
+  {
+    const int vrow = 4 * gq + (li >> 2);
+#pragma unroll
+    for (int dt = 0; dt < C::kDT; ++dt)
+      voff[dt] = C::kKBytes + vrow * C::kRowBytes + (((dt * 2 + ((li & 3) >> 1)) ^ (vrow & C::kSwz)) * 16) +
+                 (li & 1) * 8;
+  }
+
+  // One chunk of this wave's work; `masked` (a compile-time tag) selects
+  // the copy with the causal mask, used only where some key of the chunk
+  // lies past some row of the wave.
+  auto chunk_work = [&](const char* st, int k0, auto masked) __attribute__((always_inline)) {
       // S^T tiles: keys kt*16 + (4*gq + r), query li
       floatx4 sv[QT][4];
 #pragma unroll
-      for (int qt = 0; qt < QT; ++qt)
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt) sv[qt][kt] = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
-        const int key = kt * 16 + li;
 #pragma unroll
         for (int ks = 0; ks < C::kKS; ++ks) {
-          const int c = gq * C::kKS + ks;
           bf16x8 ka;
-          __builtin_memcpy(&ka, st + key * C::kRowBytes + ((c ^ (key & C::kSwz)) * 16), 16);
+          __builtin_memcpy(&ka, st + koff[ks] + kt * 16 * C::kRowBytes, 16);
 #pragma unroll
           for (int qt = 0; qt < QT; ++qt) {
             bf16x8 qb;
             __builtin_memcpy(&qb, &qop[qt][ks], 16);
-            sv[qt][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qb, sv[qt][kt], 0, 0, 0);
+            sv[qt][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                ka, qb, ks == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : sv[qt][kt], 0, 0, 0);
           }
         }
+      }
+      // causal mask, only in chunks where some key lies past some row of this wave
+      if constexpr (decltype(masked)::value) {
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt)
+#pragma unroll
+          for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (k0 + kt * 16 + 4 * gq + r > qpos[qt]) sv[qt][kt][r] = kNegInf;
       }
       // online softmax per query (lane's query li of each tile), in log2 units
       bf16x8 pb[QT][2];
@@ -248,17 +265,14 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            if (diag && k0 + kt * 16 + 4 * gq + r > qpos[qt]) sv[qt][kt][r] = kNegInf;
-            cmax = fmaxf(cmax, sv[qt][kt][r]);
-          }
+          for (int r = 0; r < 4; ++r) cmax = fmaxf(cmax, sv[qt][kt][r]);
         cmax = wave_max4(cmax) * a.c;
         // the reference m is raised only when some row's maximum passes it
         // by more than kHeadroom; otherwise weights up to 2^kHeadroom are
         // accumulated as they are (the decision is per wave)
         if (__ballot(cmax > m[qt] + kHeadroom) != 0ull) {
           const float mn = fmaxf(m[qt], cmax);
-          const float alpha = exp2f(m[qt] - mn);
+          const float alpha = __builtin_amdgcn_exp2f(m[qt] - mn);
           m[qt] = mn;
           l[qt] *= alpha;
 #pragma unroll
@@ -270,7 +284,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(AttnArgs a) {
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const float p = exp2f(fmaf(sv[qt][kt][r], a.c, -mr));
+            const float p = __builtin_amdgcn_exp2f(fmaf(sv[qt][kt][r], a.c, -mr));
             lsum += p;
             pb[qt][kt >> 1][(kt & 1) * 4 + r] = (__bf16)p;
           }
@@ -280,16 +294,12 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(AttnArgs a) {
       // the transposed load, keys 32j + 4gq + (li >> 2) (+16) at head-dim
       // columns dt*16 + 4*(li & 3) .. +3 and receives four keys at column
       // dt*16 + li
-      const char* vs = st + C::kKBytes;
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
 #pragma unroll
         for (int dt = 0; dt < C::kDT; ++dt) {
-          const int c = dt * 2 + ((li & 3) >> 1);
-          const int key1 = 32 * j + 4 * gq + (li >> 2);
-          const int key2 = key1 + 16;
-          const v4i16 lo = read_tr(vs + key1 * C::kRowBytes + ((c ^ (key1 & C::kSwz)) * 16) + (li & 1) * 8);
-          const v4i16 hi = read_tr(vs + key2 * C::kRowBytes + ((c ^ (key2 & C::kSwz)) * 16) + (li & 1) * 8);
+          const v4i16 lo = read_tr(st + voff[dt] + (32 * j) * C::kRowBytes);
+          const v4i16 hi = read_tr(st + voff[dt] + (32 * j + 16) * C::kRowBytes);
           bf16x8 va;
           __builtin_memcpy(&va, &lo, 8);
           __builtin_memcpy((char*)&va + 8, &hi, 8);
@@ -298,9 +308,27 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(AttnArgs a) {
             o[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[qt][j], o[qt][dt], 0, 0, 0);
         }
       }
-    }
+  };
+
+  // Every wave passes the same barriers chunk by chunk; a wave works on the
+  // chunks up to its last row's position, with the causal mask from the
+  // first chunk in which some key lies past its first row.  Two loops over
+  // the same step keep the unmasked code free of the mask.
+  auto step = [&](int ch, auto masked) __attribute__((always_inline)) {
+    wait_copies();
+    lds_barrier();
+    if (ch + 1 < n_chunks) issue(ch + 1);
+    int next_page = 0;
+    if (wave == 0 && ch + 2 < n_chunks) next_page = page_of(ch + 2);
+    const int k0 = ch * kKeys;
+    if (k0 <= wave_last_pos) chunk_work(smem + (ch % C::kStages) * C::kStage, k0, masked);
     if (wave == 0 && ch + 2 < n_chunks) put_offset(ch + 2, next_page);
-  }
+  };
+  // first chunk whose last key passes this wave's first row position
+  const int first_masked = min(n_chunks, wave_first_pos >= kKeys - 1 ? (wave_first_pos - (kKeys - 1)) / kKeys + 1 : 0);
+  int ch = 0;
+  for (; ch < first_masked; ++ch) step(ch, std::false_type{});
+  for (; ch < n_chunks; ++ch) step(ch, std::true_type{});
 
   // ---- normalise and store: lane holds O^T[dt*16 + 4*gq + r][query li] ----
 #pragma unroll
