@@ -30,6 +30,9 @@
  * (p0 + window > seq_len), or a page of [0, p0 + window) outside the pool.
  * A flagged sequence's outputs are left unwritten.  bf16 only
  * (params.dtype = KARA_BF16, else KARA_ERR_UNSUPPORTED), head_dim 64 or 128.
+ * Device arrays are 16-byte aligned.  kara_recompute_queries creates one
+ * rocBLAS handle per device on its first call there; rocBLAS allocates that
+ * handle's own workspace.
  *
  * Layouts (row-major)
  *   q, out (attention)  [n_trig][window][n_q_heads][head_dim] bf16
@@ -56,8 +59,8 @@ extern "C" {
 #endif
 
 typedef struct kara_model {
-  int32_t hidden;      /* model width D */
-  int32_t ffn;         /* feed-forward width F */
+  int32_t hidden;      /* model width D, a multiple of 4 */
+  int32_t ffn;         /* feed-forward width F, a multiple of 8 */
   float rope_theta;    /* rotary base */
   float rms_eps;       /* RMSNorm epsilon (inside the square root) */
 } kara_model_t;

@@ -21,8 +21,9 @@ kara_status_t recompute_geom(const kara_params_t* p, int32_t n_trig, Geom* g) {
   return KARA_OK;
 }
 
+// vectorised element-wise kernels: hidden a multiple of 4, ffn of 8
 bool model_ok(const kara_model_t* m) {
-  return m && m->hidden >= 1 && m->ffn >= 1 && m->rope_theta > 1.f && std::isfinite(m->rope_theta) &&
+  return m && m->hidden >= 4 && m->hidden % 4 == 0 && m->ffn >= 8 && m->ffn % 8 == 0 && m->rope_theta > 1.f && std::isfinite(m->rope_theta) &&
          m->rms_eps >= 0.f && std::isfinite(m->rms_eps);
 }
 
