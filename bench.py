@@ -20,6 +20,7 @@ sample of units on this host.
     python bench.py --workload soak [--intervals n] [--warmup W]
     python bench.py --workload serve [--requests n]
     python bench.py --workload recompute [--steps K] [--warmup W]
+    python bench.py --workload regions
 
 The soak runs the compression step inside a decode loop (append, decode
 attention, compress, reclaim pages; paper_2607_01237_amd/soak.py) and reports
@@ -521,6 +522,48 @@ def run_recompute(args):
     print(json.dumps(result), flush=True)
 
 
+def run_regions(args):
+    """Survivors per region of the original sequence under Kara's windows and
+    under the threshold-triggered whole-cache top-k (the analogue of the
+    paper's Fig. 2), at the serving settings of App. B.1: windows of 768
+    tokens with a 32-token buffer keeping 257, against compressing the whole
+    cache to 1025 tokens whenever it reaches 1280 (32 observation tokens).
+    4 sequences x 4 layers of an 8B shape, 8192 generated tokens each."""
+    import torch
+
+    from paper_2607_01237_amd import kara, regions
+
+    kara.load()
+    device = torch.device("cuda:0")
+    torch.cuda.set_device(device)
+    shape = dict(n_layers=4, n_q_heads=32, n_kv_heads=8, head_dim=128)
+    geos = {
+        "kara": dict(window=768, buffer=32, budget=225, chunk_budget=16, max_chunk_len=8, block_size=16),
+        "threshold": dict(window=1280, buffer=32, budget=993, chunk_budget=0, max_chunk_len=8, block_size=16,
+                          score_queries=32),
+    }
+    n_tok, region = 8192, 512
+    t0 = time.perf_counter()
+    out = regions.run(shape, geos, n_seqs=4, n_tokens=n_tok, chunk=128, region=region, device=device, seed=12,
+                      check_every=4)
+    wall = time.perf_counter() - t0
+    rows = {pol: [dict(tokens=g, survivors=[round(x, 1) for x in row]) for g, row in v["events"]]
+            for pol, v in out.items()}
+    result = {
+        "metric": "cached tokens per 512-token region of the original sequence after repeated compression",
+        "value": out["kara"]["final"][0], "unit": "tokens of region 0 still cached (Kara)",
+        "n_gpus": 1, "steps": len(rows["kara"]), "warmup": 0, "ms_per_step": wall * 1e3 / max(1, len(rows["kara"])),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) K/V and queries; V rows carry their token index)",
+        "config": {"workload": "regions", "sequences": 4, "layers": 4, "q_heads": 32, "kv_heads": 8, "head_dim": 128,
+                   "generated_tokens": n_tok, "region": region, **{f"{p}_{k}": v for p, g in geos.items()
+                                                                   for k, v in g.items()}},
+        "regions": {pol: {"events": len(rows[pol]), "final": [round(x, 1) for x in out[pol]["final"]],
+                          "cache_len": out[pol]["cache_len"], "per_event": rows[pol]} for pol in out},
+    }
+    print(json.dumps(result), flush=True)
+
+
 def run_serve(args):
     """The serving analogue of the paper's throughput runs (App. B.1): a batch
     of requests served to completion by the periodic policy on a memory-bound
@@ -612,6 +655,9 @@ def main():
         return
     if args.workload == "recompute":
         run_recompute(args)
+        return
+    if args.workload == "regions":
+        run_regions(args)
         return
     import torch
 
