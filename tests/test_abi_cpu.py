@@ -137,3 +137,36 @@ def test_scoring_queries_shrink_the_workspace(lib):
     part = kara.workspace_size(good_params(buffer=64, budget=192, score_queries=64), 8, 1)
     assert part < full
     assert kara.workspace_size(good_params(score_queries=1024), 8, 1) == full
+
+
+def test_recompute_host_checks(lib):
+    """The recompute entry points reject bad arguments on the host (nothing
+    is launched) and accept empty calls."""
+    p = good_params()
+    m = kara.make_model(4096, 12288)
+    assert kara.recompute_workspace_size(p, m, 4) > 0
+    assert kara.recompute_workspace_size(p, m, 8) > kara.recompute_workspace_size(p, m, 4)
+    for bad in (kara.make_model(4094, 12288), kara.make_model(4096, 12284), kara.make_model(4096, 12288, 0.5),
+                kara.make_model(4096, 12288, 1e4, -1.0)):
+        with pytest.raises(kara.KaraError) as e:
+            kara.recompute_workspace_size(p, bad, 4)
+        assert e.value.code == kara.ERR_INVALID_ARG
+    f32 = good_params(dtype="f32", window=256, budget=52)
+    with pytest.raises(kara.KaraError) as e:
+        kara.recompute_workspace_size(f32, m, 4)
+    assert e.value.code == kara.ERR_UNSUPPORTED
+    import ctypes
+    out = ctypes.c_size_t(0)
+    assert lib.kara_recompute_workspace_size(ctypes.byref(p), ctypes.byref(m), 4, None) == kara.ERR_INVALID_ARG
+    # empty calls succeed without touching the device; missing pointers are argument errors
+    assert lib.kara_recompute_attention(ctypes.byref(p), 0, None, None, None, None, None, None, None, None, None,
+                                        None) == kara.OK
+    assert lib.kara_recompute_attention(ctypes.byref(p), 2, None, None, None, None, None, None, None, None, None,
+                                        None) == kara.ERR_INVALID_ARG
+    w = (kara.LayerWeights * 1)()
+    assert lib.kara_recompute_queries(ctypes.byref(p), ctypes.byref(m), 0, None, 1, w, None, None, None, None, None,
+                                      None, None, None, None, None, None, 0, None) == kara.OK
+    assert lib.kara_recompute_queries(ctypes.byref(p), ctypes.byref(m), 2, None, 1, w, None, None, None, None, None,
+                                      None, None, None, None, None, None, 0, None) == kara.ERR_INVALID_ARG
+    assert lib.kara_recompute_queries(ctypes.byref(p), ctypes.byref(m), 2, None, 0, w, None, None, None, None, None,
+                                      None, None, None, None, None, None, 0, None) == kara.ERR_INVALID_ARG
