@@ -58,14 +58,49 @@ __device__ inline double chunk_score(float a_lo, float a_hi, int gap) {
   return s * (double)(gap - 1);
 }
 
-__device__ inline uint32_t wave_incl_scan(uint32_t v) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t n = __shfl_up(v, o, 64);
-    if (lane >= o) v += n;
+// Cross-lane steps use DPP row operations (16-lane rows, a few cycles each)
+// and readlane, not LDS-routed shuffles.
+constexpr int kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118;
+constexpr int kDppQuadXor1 = 0xB1, kDppQuadXor2 = 0x4E, kDppRowHalfMirror = 0x141, kDppRowMirror = 0x140;
+
+__device__ inline uint32_t dpp_u32(uint32_t v, int ctrl) {
+  switch (ctrl) {
+    case kDppRowShr1: return __builtin_amdgcn_update_dpp(0u, v, kDppRowShr1, 0xf, 0xf, true);
+    case kDppRowShr2: return __builtin_amdgcn_update_dpp(0u, v, kDppRowShr2, 0xf, 0xf, true);
+    case kDppRowShr4: return __builtin_amdgcn_update_dpp(0u, v, kDppRowShr4, 0xf, 0xf, true);
+    case kDppRowShr8: return __builtin_amdgcn_update_dpp(0u, v, kDppRowShr8, 0xf, 0xf, true);
+    case kDppQuadXor1: return __builtin_amdgcn_update_dpp(0u, v, kDppQuadXor1, 0xf, 0xf, true);
+    case kDppQuadXor2: return __builtin_amdgcn_update_dpp(0u, v, kDppQuadXor2, 0xf, 0xf, true);
+    case kDppRowHalfMirror: return __builtin_amdgcn_update_dpp(0u, v, kDppRowHalfMirror, 0xf, 0xf, true);
+    default: return __builtin_amdgcn_update_dpp(0u, v, kDppRowMirror, 0xf, 0xf, true);
   }
-  return v;
+}
+
+// Inclusive prefix sum over the 64 lanes: within each 16-lane row by
+// shifted adds (lanes shifted in from outside the row read 0), then each
+// row adds the totals of the rows before it.
+__device__ inline uint32_t wave_incl_scan(uint32_t v) {
+  v += dpp_u32(v, kDppRowShr1);
+  v += dpp_u32(v, kDppRowShr2);
+  v += dpp_u32(v, kDppRowShr4);
+  v += dpp_u32(v, kDppRowShr8);
+  const uint32_t r0 = __builtin_amdgcn_readlane(v, 15), r1 = __builtin_amdgcn_readlane(v, 31),
+                 r2 = __builtin_amdgcn_readlane(v, 47);
+  const int row = (threadIdx.x & 63) >> 4;
+  return v + (row >= 1 ? r0 : 0u) + (row >= 2 ? r1 : 0u) + (row >= 3 ? r2 : 0u);
+}
+
+// Maximum over the 64 lanes, the same in every lane: a butterfly within
+// each row (neighbours, pairs, the row's mirror halves), then the four rows.
+__device__ inline uint32_t umax32(uint32_t a, uint32_t b) { return a > b ? a : b; }
+
+__device__ inline uint32_t wave_max_u32(uint32_t v) {
+  v = umax32(v, dpp_u32(v, kDppQuadXor1));
+  v = umax32(v, dpp_u32(v, kDppQuadXor2));
+  v = umax32(v, dpp_u32(v, kDppRowHalfMirror));
+  v = umax32(v, dpp_u32(v, kDppRowMirror));
+  return umax32(umax32((uint32_t)__builtin_amdgcn_readlane(v, 0), (uint32_t)__builtin_amdgcn_readlane(v, 16)),
+                umax32((uint32_t)__builtin_amdgcn_readlane(v, 32), (uint32_t)__builtin_amdgcn_readlane(v, 48)));
 }
 
 // Exclusive prefix sum over threads in index order; *total = block sum.
@@ -173,15 +208,18 @@ __device__ void argmax_top(const KeyT (&key)[kSelEpt], const bool (&elig)[kSelEp
         bk = (uint64_t)key[e];
         bp = base + e;
       }
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      const uint32_t lo = __shfl_xor((uint32_t)bk, o, 64), hi = __shfl_xor((uint32_t)(bk >> 32), o, 64);
-      const uint64_t ok = ((uint64_t)hi << 32) | lo;
-      const int op = __shfl_xor(bp, o, 64);
-      if (beats(ok, op, bk, bp)) {
-        bk = ok;
-        bp = op;
-      }
+    // the wave's best: the largest key (high word, then low word among the
+    // lanes holding the largest high word), then the lowest lane holding it;
+    // lanes own ascending blocks of positions, so that lane's position is
+    // the lowest among equal keys
+    {
+      const uint32_t hi = wave_max_u32((uint32_t)(bk >> 32));
+      const uint32_t lo = wave_max_u32((uint32_t)(bk >> 32) == hi ? (uint32_t)bk : 0u);
+      const uint64_t wk = ((uint64_t)hi << 32) | lo;
+      const uint64_t owners = __ballot(bk == wk);
+      const int src = (int)__builtin_ctzll(owners);
+      bk = wk;
+      bp = __builtin_amdgcn_readlane(bp, src);
     }
     const int slot = r & 1;
     if (lane == 0) {
