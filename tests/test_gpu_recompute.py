@@ -224,3 +224,39 @@ def test_recompute_pass_layers(window, n_q, n_kv, d, D, F, bs):
         assert torch.equal(q_all[l].view(torch.int16), q_layers[l].view(torch.int16)), f"layer {l} queries"
     assert torch.equal(h_all, h)
     print("[case] ok", flush=True)
+
+
+def test_recompute_then_compress():
+    """The event pipeline: the recompute pass writes the scoring queries of
+    every layer, kara_compress_window consumes them, and the result passes
+    P1-P4 against the oracle run on the same queries (the layouts of the
+    two entry points agree)."""
+    import kara_check as kc
+    from paper_2607_01237_amd import kara
+    _need_gpu()
+    print("\n[case] recompute -> compress", flush=True)
+    c = kc.setup(ki.workload("batch8", n_seqs=3, n_layers=2, window=128, budget=26, n_q_heads=8, n_kv_heads=2,
+                             prefix=(10, 100), tail=(0, 8), num_pages=None, pool_slack=0.25))
+    p = c.p
+    L, nt = len(c.kp), c.trig.numel()
+    W, Hq, d = p["window"], p["n_q_heads"], p["head_dim"]
+    D, F = 256, 512
+    dev = c.q.device
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    wts = _weights(g, L, D, F, Hq * d, dev)
+    model = kara.make_model(D, F, rope_theta=1e6, rms_eps=1e-6)
+    h0 = torch.randn((nt, W, D), generator=g, device=dev)
+    h1 = torch.empty_like(h0)
+    q = torch.empty((L, nt, W, Hq, d), dtype=torch.bfloat16, device=dev)
+    status = torch.full((nt,), -7, dtype=torch.int32, device=dev)
+    wsp = torch.empty(kara.recompute_workspace_size(c.params, model, nt), dtype=torch.uint8, device=dev)
+    kara.recompute_queries(c.params, model, c.trig, wts, h0, h1, c.kp, c.vp, c.bt, c.seq_lens, c.win_start,
+                           c.win_start, q, status, wsp)
+    torch.cuda.synchronize()
+    assert (status.cpu().numpy() == 0).all()
+    assert torch.isfinite(q.float()).all()
+    c.q = q
+    c.host["q"] = ki.raw_numpy(q)
+    rep, _ = kc.full_check(c)
+    print(f"[case] ok {rep}", flush=True)
