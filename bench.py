@@ -144,10 +144,10 @@ def summarize_pmc(fetch_csv, write_csv, workload, calib_gib):
     sf, sw = true_bytes / cf, true_bytes / cw
     lines = [f"# HBM traffic from rocprofv3 counters: {workload} workload", "",
              "Two counter runs of the same command, one per counter block:", "", "```",
-             f"cd /tmp && export TMPDIR=/tmp && rocprofv3 --pmc FETCH_SIZE -d $REPO/gpurun_out/pmc_fetch -o pmc "
+             f"cd /tmp && export TMPDIR=/tmp && rocprofv3 --pmc FETCH_SIZE -d $OUT/pmc_fetch -o pmc "
              f"--output-format csv -- python3 $REPO/bench.py --workload {workload} --steps 1 --warmup 0 "
              f"--no-cpu-baseline --copy-calibration-gib {calib_gib:g}",
-             "(the same with --pmc WRITE_SIZE and -d $REPO/gpurun_out/pmc_write)",
+             "(the same with --pmc WRITE_SIZE and -d $OUT/pmc_write; $OUT is any output directory)",
              f"python3 bench.py --workload {workload} --copy-calibration-gib {calib_gib:g} "
              "--summarize-pmc <fetch csv> <write csv>", "```", "",
              f"Calibration: one bf16 negation over {calib_gib:g} GiB reads and writes {true_bytes / 1e9:.3f} GB; the "
@@ -644,8 +644,8 @@ def main():
                             args.copy_calibration_gib or 1.0))
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 (multi-GPU sharding is "
-                                   "described in DESIGN.md and not built)"}))
+        print(json.dumps({"error": "this benchmark runs on one GPU; --gpus must be 1 (the step needs no "
+                                   "communication: sequences or KV heads would be split across GPUs, not built here)"}))
         sys.exit(2)
     if args.workload == "soak":
         run_soak(args)

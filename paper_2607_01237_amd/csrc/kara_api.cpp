@@ -201,7 +201,7 @@ const char* kara_status_string(int32_t s) {
   switch (s) {
     case KARA_OK: return "KARA_OK";
     case KARA_ERR_INVALID_ARG: return "KARA_ERR_INVALID_ARG: a parameter is out of range or a pointer is NULL";
-    case KARA_ERR_UNSUPPORTED: return "KARA_ERR_UNSUPPORTED: valid parameters this build does not support";
+    case KARA_ERR_UNSUPPORTED: return "KARA_ERR_UNSUPPORTED: valid parameters libkara does not support";
     case KARA_ERR_WORKSPACE: return "KARA_ERR_WORKSPACE: workspace missing or too small";
     case KARA_ERR_HIP: return "KARA_ERR_HIP: the HIP runtime rejected a launch";
     case -5: return "KARA_ERR_SCHED_MISMATCH: the device's freed pages differ from the scheduler's";
