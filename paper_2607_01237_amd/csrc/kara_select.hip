@@ -11,7 +11,10 @@ namespace kara {
 namespace {
 
 constexpr int kSelThreads = 256;
-constexpr int kSelEpt = KARA_MAX_COMPRESSIBLE / kSelThreads;  // positions per thread, at most
+constexpr int kSelEptMax = KARA_MAX_COMPRESSIBLE / kSelThreads;  // positions per thread, at most
+// Kernel instances: EPT positions per thread, 8 (windows of up to 2048
+// compressible positions) or EPTMax; the smaller arrays keep more
+// units in flight.
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr uint32_t kArgmaxMax = 8;   // selections of at most this many items use argmax rounds
 
@@ -125,8 +128,8 @@ __device__ uint32_t block_excl_scan(uint32_t v, SelFixed& f, uint32_t* total) {
 // position first among equal keys -- where thread i owns positions
 // [i*ept, i*ept+ept).  MSB-first radix select over 8-bit digits finds the
 // K-th key; items equal to it are then taken in position order.
-template <typename KeyT>
-__device__ void radix_top(const KeyT (&key)[kSelEpt], const bool (&elig)[kSelEpt], bool (&sel)[kSelEpt],
+template <int EPT, typename KeyT>
+__device__ void radix_top(const KeyT (&key)[EPT], const bool (&elig)[EPT], bool (&sel)[EPT],
                           uint32_t K, SelFixed& f) {
   constexpr int kBits = sizeof(KeyT) * 8;
   const int tid = threadIdx.x;
@@ -141,7 +144,7 @@ __device__ void radix_top(const KeyT (&key)[kSelEpt], const bool (&elig)[kSelEpt
     // scores): add runs of equal digits with one atomic
     uint32_t run_bin = 0, run = 0;
 #pragma unroll
-    for (int e = 0; e < kSelEpt; ++e) {
+    for (int e = 0; e < EPT; ++e) {
       if (!elig[e]) continue;
       const bool match = (shift == kBits - 8) || (((key[e] ^ prefix) >> (shift + 8)) == 0);
       if (!match) continue;
@@ -173,11 +176,11 @@ __device__ void radix_top(const KeyT (&key)[kSelEpt], const bool (&elig)[kSelEpt
   }
   uint32_t eq = 0;
 #pragma unroll
-  for (int e = 0; e < kSelEpt; ++e) eq += (elig[e] && key[e] == prefix) ? 1u : 0u;
+  for (int e = 0; e < EPT; ++e) eq += (elig[e] && key[e] == prefix) ? 1u : 0u;
   uint32_t tot;
   uint32_t rank = block_excl_scan(eq, f, &tot);
 #pragma unroll
-  for (int e = 0; e < kSelEpt; ++e) {
+  for (int e = 0; e < EPT; ++e) {
     const bool is_eq = elig[e] && key[e] == prefix;
     sel[e] = (elig[e] && key[e] > prefix) || (is_eq && rank < remaining);
     rank += is_eq ? 1u : 0u;
@@ -191,19 +194,19 @@ __device__ inline bool beats(uint64_t ka, int pa, uint64_t kb, int pb) {
 
 // The same selection as radix_top for small K: K rounds, each taking the best
 // remaining item (a block argmax over (key desc, position asc)).
-template <typename KeyT>
-__device__ void argmax_top(const KeyT (&key)[kSelEpt], const bool (&elig)[kSelEpt], bool (&sel)[kSelEpt],
+template <int EPT, typename KeyT>
+__device__ void argmax_top(const KeyT (&key)[EPT], const bool (&elig)[EPT], bool (&sel)[EPT],
                            uint32_t K, int base, SelFixed& f) {
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
 #pragma unroll
-  for (int e = 0; e < kSelEpt; ++e) sel[e] = false;
+  for (int e = 0; e < EPT; ++e) sel[e] = false;
   for (uint32_t r = 0; r < K; ++r) {
     // this thread's best: positions ascend with e, so the first maximum wins ties
     uint64_t bk = 0;
     int bp = 0x7fffffff;
 #pragma unroll
-    for (int e = 0; e < kSelEpt; ++e)
+    for (int e = 0; e < EPT; ++e)
       if (elig[e] && !sel[e] && beats((uint64_t)key[e], base + e, bk, bp)) {
         bk = (uint64_t)key[e];
         bp = base + e;
@@ -240,28 +243,29 @@ __device__ void argmax_top(const KeyT (&key)[kSelEpt], const bool (&elig)[kSelEp
     // are never eligible)
     const int e = gp - base;
 #pragma unroll
-    for (int i = 0; i < kSelEpt; ++i)
+    for (int i = 0; i < EPT; ++i)
       if (i == e && elig[i]) sel[i] = true;
   }
 }
 
-template <typename KeyT>
-__device__ void select_top(const KeyT (&key)[kSelEpt], const bool (&elig)[kSelEpt], bool (&sel)[kSelEpt],
+template <int EPT, typename KeyT>
+__device__ void select_top(const KeyT (&key)[EPT], const bool (&elig)[EPT], bool (&sel)[EPT],
                            uint32_t K, int base, SelFixed& f) {
   uint32_t cnt = 0;
 #pragma unroll
-  for (int e = 0; e < kSelEpt; ++e) cnt += elig[e] ? 1u : 0u;
+  for (int e = 0; e < EPT; ++e) cnt += elig[e] ? 1u : 0u;
   uint32_t n_el;
   block_excl_scan(cnt, f, &n_el);
   if (K >= n_el || K == 0) {
 #pragma unroll
-    for (int e = 0; e < kSelEpt; ++e) sel[e] = K != 0 && elig[e];
+    for (int e = 0; e < EPT; ++e) sel[e] = K != 0 && elig[e];
     return;
   }
-  if (K <= kArgmaxMax) argmax_top(key, elig, sel, K, base, f);
-  else radix_top(key, elig, sel, K, f);
+  if (K <= kArgmaxMax) argmax_top<EPT>(key, elig, sel, K, base, f);
+  else radix_top<EPT>(key, elig, sel, K, f);
 }
 
+template <int EPT>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
     Geom g, int mode, const float* __restrict__ scores, const int32_t* __restrict__ disc_in,
     int32_t* __restrict__ disc_out, int32_t* __restrict__ kept_out) {
@@ -286,25 +290,25 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
 
   const int ept = (N + kSelThreads - 1) / kSelThreads;
   const int base = tid * ept;
-  uint32_t key[kSelEpt];
-  bool elig[kSelEpt], sel[kSelEpt];
+  uint32_t key[EPT];
+  bool elig[EPT], sel[EPT];
 
   if (mode & kSelectDiscrete) {
     // Eq. (5): the budget - alpha best positions, kept ascending
 #pragma unroll
-    for (int e = 0; e < kSelEpt; ++e) {
+    for (int e = 0; e < EPT; ++e) {
       const int j = base + e;
       elig[e] = e < ept && j < N;
       key[e] = elig[e] ? ord32(sm.a[j]) : 0u;
     }
-    select_top(key, elig, sel, (uint32_t)k, base, f);
+    select_top<EPT>(key, elig, sel, (uint32_t)k, base, f);
     uint32_t c = 0;
 #pragma unroll
-    for (int e = 0; e < kSelEpt; ++e) c += sel[e] ? 1u : 0u;
+    for (int e = 0; e < EPT; ++e) c += sel[e] ? 1u : 0u;
     uint32_t tot;
     uint32_t r = block_excl_scan(c, f, &tot);
 #pragma unroll
-    for (int e = 0; e < kSelEpt; ++e)
+    for (int e = 0; e < EPT; ++e)
       if (sel[e]) {
         const int j = base + e;
         sm.disc[r] = j;
@@ -339,10 +343,10 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     const int nc = k - 1;
     const int ept2 = (nc + kSelThreads - 1) / kSelThreads;
     const int base2 = tid * ept2;
-    uint64_t key2[kSelEpt];
-    bool el2[kSelEpt], s2[kSelEpt];
+    uint64_t key2[EPT];
+    bool el2[EPT], s2[EPT];
 #pragma unroll
-    for (int e = 0; e < kSelEpt; ++e) {
+    for (int e = 0; e < EPT; ++e) {
       const int i = base2 + e;
       el2[e] = false;
       key2[e] = 0;
@@ -355,9 +359,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
         }
       }
     }
-    select_top(key2, el2, s2, (uint32_t)g.n_chunks, base2, f);
+    select_top<EPT>(key2, el2, s2, (uint32_t)g.n_chunks, base2, f);
 #pragma unroll
-    for (int e = 0; e < kSelEpt; ++e)
+    for (int e = 0; e < EPT; ++e)
       if (s2[e]) {
         const int i = base2 + e;
         const int lo = sm.disc[i], hi = sm.disc[i + 1];
@@ -372,14 +376,14 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   const int fill = g.alpha - (int)added;
   if (fill > 0) {
 #pragma unroll
-    for (int e = 0; e < kSelEpt; ++e) {
+    for (int e = 0; e < EPT; ++e) {
       const int j = base + e;
       elig[e] = e < ept && j < N && sm.mark[j] == 0;
       key[e] = elig[e] ? ord32(sm.a[j]) : 0u;
     }
-    select_top(key, elig, sel, (uint32_t)fill, base, f);
+    select_top<EPT>(key, elig, sel, (uint32_t)fill, base, f);
 #pragma unroll
-    for (int e = 0; e < kSelEpt; ++e)
+    for (int e = 0; e < EPT; ++e)
       if (sel[e]) sm.mark[base + e] |= 4;
   }
   __syncthreads();
@@ -387,14 +391,14 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   // the kept set, ascending
   uint32_t c = 0;
 #pragma unroll
-  for (int e = 0; e < kSelEpt; ++e) {
+  for (int e = 0; e < EPT; ++e) {
     const int j = base + e;
     if (e < ept && j < N && sm.mark[j]) ++c;
   }
   uint32_t tot;
   uint32_t r = block_excl_scan(c, f, &tot);
 #pragma unroll
-  for (int e = 0; e < kSelEpt; ++e) {
+  for (int e = 0; e < EPT; ++e) {
     const int j = base + e;
     if (e < ept && j < N && sm.mark[j]) kept_out[u * g.budget + r++] = j;
   }
@@ -406,8 +410,12 @@ hipError_t launch_select(const Geom& g, int64_t n_units, int mode, const float* 
                          const int32_t* discrete_in, int32_t* discrete_out, int32_t* kept_out,
                          hipStream_t stream) {
   if (n_units <= 0) return hipSuccess;
-  hipLaunchKernelGGL(select_kernel, dim3((unsigned)n_units), dim3(kSelThreads), sel_lds_bytes(g.N), stream, g,
-                     mode, scores, discrete_in, discrete_out, kept_out);
+  if (g.N <= 8 * kSelThreads)
+    hipLaunchKernelGGL(select_kernel<8>, dim3((unsigned)n_units), dim3(kSelThreads), sel_lds_bytes(g.N), stream, g,
+                       mode, scores, discrete_in, discrete_out, kept_out);
+  else
+    hipLaunchKernelGGL(select_kernel<kSelEptMax>, dim3((unsigned)n_units), dim3(kSelThreads), sel_lds_bytes(g.N),
+                       stream, g, mode, scores, discrete_in, discrete_out, kept_out);
   return hipGetLastError();
 }
 
