@@ -64,6 +64,8 @@ def parse():
     ap.add_argument("--copy-calibration-gib", type=float, default=0.0,
                     help="run one plain streaming kernel (bf16 negation) over this many GiB before the steps, as "
                          "the reference for rocprofv3 FETCH_SIZE / WRITE_SIZE counts")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="CSV",
+                    help="print the per-kernel mean per dispatch of every counter in rocprofv3 --pmc CSVs, and exit")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print the HBM-traffic summary of two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) "
                          "of this script with --copy-calibration-gib, and exit")
@@ -133,13 +135,15 @@ def summarize_pmc(fetch_csv, write_csv, workload, calib_gib):
     write, wnames = _pmc_per_dispatch(write_csv, "WRITE_SIZE")
     true_bytes = calib_gib * 2**30
 
-    def per_kernel(per, nm, key):
+    def total_of(per, nm, key):
         vals = [v * 1024.0 for d, v in per.items() if key in nm[d]]   # counters are KiB per dispatch
-        return float(np.median(vals)) if vals else None, len(vals)
+        return float(np.sum(vals)), len(vals)
 
-    cf, _ = per_kernel(fetch, names, CALIBRATION_KERNEL)
-    cw, _ = per_kernel(write, wnames, CALIBRATION_KERNEL)
-    if not cf or not cw:
+    # torch splits the negation of more than 2^31 elements into several
+    # dispatches: the calibration is the total over all of them
+    cf, ncf = total_of(fetch, names, CALIBRATION_KERNEL)
+    cw, ncw = total_of(write, wnames, CALIBRATION_KERNEL)
+    if not ncf or not ncw:
         raise SystemExit("the calibration kernel is missing from the counter runs (use --copy-calibration-gib)")
     sf, sw = true_bytes / cf, true_bytes / cw
     lines = [f"# HBM traffic from rocprofv3 counters: {workload} workload", "",
@@ -150,14 +154,11 @@ def summarize_pmc(fetch_csv, write_csv, workload, calib_gib):
              "(the same with --pmc WRITE_SIZE and -d $OUT/pmc_write; $OUT is any output directory)",
              f"python3 bench.py --workload {workload} --copy-calibration-gib {calib_gib:g} "
              "--summarize-pmc <fetch csv> <write csv>", "```", "",
-             f"Calibration: one bf16 negation over {calib_gib:g} GiB reads and writes {true_bytes / 1e9:.3f} GB; the "
+             f"Calibration: one bf16 negation over {calib_gib:g} GiB ({ncf} dispatches) reads and writes "
+             f"{true_bytes / 1e9:.3f} GB; the "
              f"counters read {cf / 1e9:.3f} GB fetched and {cw / 1e9:.3f} GB written, so FETCH_SIZE is scaled by "
              f"{sf:.4f} and WRITE_SIZE by {sw:.4f}.", "",
              "| kernel | dispatches | FETCH (GB, scaled) | WRITE (GB, scaled) |", "|---|---|---|---|"]
-    def total_of(per, nm, key):
-        vals = [v * 1024.0 for d, v in per.items() if key in nm[d]]
-        return float(np.sum(vals)), len(vals)
-
     blob = {"workload": workload, "calibration_gib": calib_gib, "fetch_scale": sf, "write_scale": sw}
     for stage, kernels in TRAFFIC_KERNELS.items():
         total = 0.0
@@ -176,6 +177,34 @@ def summarize_pmc(fetch_csv, write_csv, workload, calib_gib):
     lines += ["", "The table gives the average per dispatch.  Per pass of a stage (one scoring launch; one "
               "selection-and-compaction pass, where the bench's staged pass runs selection as two launches and "
               "the fused step as one):", "", "```json", json.dumps(blob, indent=1), "```"]
+    return "\n".join(lines)
+
+
+def summarize_counters(paths):
+    """Markdown table: for every kernel (name up to its argument list), the
+    number of dispatches and the mean per dispatch of each counter found."""
+    import csv
+    vals, disp = {}, {}
+    for path in paths:
+        per = {}
+        for r in csv.DictReader(open(path)):
+            name = r["Kernel_Name"].replace("(anonymous namespace)::", "").split("(", 1)[0].replace("void ", "")
+            name = name if len(name) <= 60 else name[:57] + "..."
+            key = (path, r["Dispatch_Id"])
+            d = per.setdefault(key, {"name": name})
+            d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+        for (p, _), d in per.items():
+            name = d.pop("name")
+            for c, v in d.items():
+                vals.setdefault(name, {}).setdefault(c, []).append(v)
+            disp.setdefault(name, {}).setdefault(p, 0)
+            disp[name][p] += 1
+    counters = sorted({c for k in vals.values() for c in k})
+    lines = ["| kernel | dispatches | " + " | ".join(counters) + " |", "|---|---|" + "---|" * len(counters)]
+    for name in sorted(vals):
+        n = max(disp[name].values())
+        cells = [f"{np.mean(vals[name][c]):.6g}" if c in vals[name] else "" for c in counters]
+        lines.append(f"| {name} | {n} | " + " | ".join(cells) + " |")
     return "\n".join(lines)
 
 
@@ -639,6 +668,9 @@ def run_serve(args):
 
 def main():
     args = parse()
+    if args.summarize_counters:
+        print(summarize_counters(args.summarize_counters))
+        return
     if args.summarize_pmc:
         print(summarize_pmc(args.summarize_pmc[0], args.summarize_pmc[1], args.workload,
                             args.copy_calibration_gib or 1.0))
@@ -762,6 +794,8 @@ def main():
     # compact+commit is its time less theirs.
     stages = ["score", "select_t2c", "compact", "commit"]
     times = {s: [] for s in stages}
+    moved = []
+    tails = (geom.seq_lens[geom.trig] - geom.win_start[geom.trig] - (nw - 1) * N - W).astype(np.int64)
     n_stage = max(3, args.steps)
     for i in range(n_stage + 1):
         restore()
@@ -788,6 +822,9 @@ def main():
             continue   # first pass warms the staged entry points
         for k, s in enumerate(stages):
             times[s].append(e[k].elapsed_time(e[k + 1]))
+        # rows this pass moved: the pools are not restored between passes, so
+        # kept rows already in place accumulate and each pass is priced alone
+        moved.append(float(moved_rows(kept.cpu().numpy().reshape(L, nt, nw, H, p["budget"]), p, tails).sum()))
     avg = {s: float(np.mean(v)) for s, v in times.items()}
     if nw > 1:
         avg["compact"] = max(0.0, avg["compact"] - avg["score"] - avg["select_t2c"])
@@ -802,9 +839,10 @@ def main():
     ach = flops / (avg["score"] * 1e-3) / 1e12
     es = 2 if p["dtype"] == "bf16" else 4
     row_bytes = p["head_dim"] * es
-    tails = (geom.seq_lens[geom.trig] - geom.win_start[geom.trig] - (nw - 1) * N - W).astype(np.int64)
-    mv = moved_rows(kept.cpu().numpy().reshape(L, nt, nw, H, p["budget"]), p, tails)
-    compact_bytes = float(mv.sum()) * row_bytes * 2 * 2          # read + write, K and V
+    # read + write, K and V, averaged over the passes timed
+    compact_bytes = float(np.mean(moved)) * row_bytes * 2 * 2
+    log("compaction algorithmic GB per staged pass (read = write): "
+        + ", ".join(f"{m * row_bytes * 2 / 1e9:.4f}" for m in moved))
     select_bytes = float(units * nw) * (N * 4 + p["budget"] * 4 + (p["budget"] - p["chunk_budget"]) * 4 * 2)
     sc_ms = avg["select_t2c"] + avg["compact"]
     sc_gbs = (compact_bytes + select_bytes) / (sc_ms * 1e-3) / 1e9
