@@ -265,3 +265,89 @@ def full_check(case: Case, commit=True, units=None):
     check_p4(case, gpu, commit)
     rep["units"] = n_units(case)
     return rep, gpu
+
+
+# ---- compaction of every unit, checked on the device against its definition ----
+# At full size the pools do not fit on the host.  Before the call, every
+# triggered sequence's rows [p0, seq_len) are copied on the device; after it,
+# each row compaction wrote must equal, bit for bit, the snapshot row the
+# compaction map names (kept ++ [N, W + tail), window-relative), and the rows
+# before p0 must keep their checksums.  Plain torch indexing, not the library.
+
+def positions(geom, lo, hi):
+    """Concatenated (page, slot) of logical positions [lo(s), hi(s)) of every
+    triggered sequence s, and each sequence's offset in the concatenation."""
+    bs = geom.params()["block_size"]
+    pg, sl, off = [], [], [0]
+    for s in geom.trig:
+        pos = np.arange(lo(int(s)), hi(int(s)), dtype=np.int64)
+        pg.append(geom.block_table[s, pos // bs].astype(np.int64))
+        sl.append(pos % bs)
+        off.append(off[-1] + len(pos))
+    return np.concatenate(pg), np.concatenate(sl), np.array(off[:-1], dtype=np.int64)
+
+
+def checksum(rows, chunk=1 << 26):
+    """Order-sensitive checksum of 16-bit rows (exact integer arithmetic, in
+    chunks to bound the temporaries)."""
+    x = rows.reshape(-1).view(torch.int16)
+    s1 = s2 = 0
+    for a in range(0, x.numel(), chunk):
+        xc = x[a:a + chunk].to(torch.int64)
+        w = torch.arange(a, a + xc.numel(), device=x.device, dtype=torch.int64) % 65521 + 1
+        s1 += int(xc.sum())
+        s2 += int((xc * w).sum())
+    return s1, s2
+
+
+class WindowSnapshot:
+    """Device copy of the rows a compression may read or move, taken before
+    the call; check() verifies every unit's compaction afterwards."""
+
+    def __init__(self, geom, kp, vp):
+        dev = kp[0].device
+        T = lambda a: torch.from_numpy(a).to(dev)
+        w_pg, w_sl, self.off = positions(geom, lambda s: int(geom.win_start[s]), lambda s: int(geom.seq_lens[s]))
+        w_pg, w_sl = T(w_pg), T(w_sl)
+        pre_pg, pre_sl, _ = positions(geom, lambda s: 0, lambda s: int(geom.win_start[s]))
+        self.pre_pg, self.pre_sl = T(pre_pg), T(pre_sl)
+        self.rows = [(k[w_pg, :, w_sl, :], v[w_pg, :, w_sl, :]) for k, v in zip(kp, vp)]
+        self.pre = [self._prefix_sums(k, v) for k, v in zip(kp, vp)]
+
+    def _prefix_sums(self, k, v):
+        return checksum(k[self.pre_pg, :, self.pre_sl, :]), checksum(v[self.pre_pg, :, self.pre_sl, :])
+
+    def check(self, geom, p, kept, kp, vp):
+        """kept: [L, n_trig, Hkv, budget] (one window per sequence)."""
+        dev = kp[0].device
+        W, N, B, bs, H = p["window"], p["window"] - p["buffer"], p["budget"], p["block_size"], p["n_kv_heads"]
+        nt = len(geom.trig)
+        trig = geom.trig.astype(np.int64)
+        p0s = geom.win_start[trig].astype(np.int64)
+        tails = geom.seq_lens[trig].astype(np.int64) - p0s - W
+        # destination j < B takes kept[j]; j >= B takes window-relative N + (j - B)
+        kt, kj = np.repeat(np.arange(nt), B), np.tile(np.arange(B), nt)
+        ex_t = np.concatenate([np.full(W + tl - N, t, dtype=np.int64) for t, tl in enumerate(tails)])
+        ex_rel = np.concatenate([np.arange(N, W + tl, dtype=np.int64) for tl in tails])
+        ex_j = ex_rel - N + B
+
+        def dst(t_idx, j):
+            pos = p0s[t_idx] + j
+            return (torch.from_numpy(geom.block_table[trig[t_idx], pos // bs].astype(np.int64)).to(dev),
+                    torch.from_numpy(pos % bs).to(dev))
+
+        k_pg, k_sl = dst(kt, kj)
+        e_pg, e_sl = dst(ex_t, ex_j)
+        e_src = torch.from_numpy(self.off[ex_t] + ex_rel).to(dev)
+        off = torch.from_numpy(self.off).to(dev).view(nt, 1, 1)
+        hv = torch.arange(H, device=dev).view(H, 1)
+        for l, (k, v) in enumerate(zip(kp, vp)):
+            src = (kept[l].to(dev).to(torch.int64) + off).permute(1, 0, 2).reshape(H, -1)    # [H, nt*B]
+            for name, pool, snap in (("K", k, self.rows[l][0]), ("V", v, self.rows[l][1])):
+                want, got = snap[src, hv], pool[k_pg.view(1, -1), hv, k_sl.view(1, -1)]
+                assert torch.equal(want.view(torch.int16), got.view(torch.int16)), \
+                    f"compaction: {name} kept rows of layer {l}"
+                want, got = snap[e_src.view(1, -1), hv], pool[e_pg.view(1, -1), hv, e_sl.view(1, -1)]
+                assert torch.equal(want.view(torch.int16), got.view(torch.int16)), \
+                    f"compaction: {name} buffer/tail rows of layer {l}"
+            assert self._prefix_sums(k, v) == self.pre[l], f"compaction: rows before the window, layer {l}"

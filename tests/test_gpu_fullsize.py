@@ -5,11 +5,16 @@ W = 2048, and the 256-sequence, 36-layer ragged one -- goes through one
 kara_compress_window call over all layers, exactly as the bench runs it.
 The oracle then checks what it can compute one unit at a time:
   P1  scores of sampled units, fp64, against the GPU's;
-  P2  the oracle's selection on the GPU's scores for a larger sample;
+  P2  the oracle's selection on the GPU's scores, for every unit;
   P3  the oracle's end-to-end kept set of the P1 units (near-ties excepted);
   P4  the compacted K/V rows of the P1 units, and the block tables, lengths
       and freed lists of every sequence.
 Only the sampled units' rows are copied to the host (the pools are ~140 GB).
+For every unit, compaction is also checked on the device against its
+definition: each row written equals, bit for bit, the row the compaction
+map names in a device snapshot of [p0, seq_len) taken before the call, and
+the rows before p0 keep their checksums.  That check uses torch indexing
+only, not the library.
 """
 import numpy as np
 import pytest
@@ -42,8 +47,8 @@ def _rows(pool, table_row, positions, head, bs):
     return ki.raw_numpy(pool[pg, head, sl, :])
 
 
-@pytest.mark.parametrize("name,n_p1,n_p2", [("qwen14b", 6, 256), ("ragged", 6, 256)])
-def test_fullsize_sampled(name, n_p1, n_p2):
+@pytest.mark.parametrize("name,n_p1", [("qwen14b", 6), ("ragged", 6)])
+def test_fullsize_sampled(name, n_p1):
     import kara_check as kc
     from paper_2607_01237_amd import kara
     _need_gpu()
@@ -81,6 +86,9 @@ def test_fullsize_sampled(name, n_p1, n_p2):
             k=_rows(kp[l], geom.block_table[s], pos, h, bs),
             v=_rows(vp[l], geom.block_table[s], pos, h, bs))
 
+    # device snapshot of every triggered sequence's [p0, seq_len), checksums of [0, p0)
+    snap = kc.WindowSnapshot(geom, kp, vp)
+
     ws = torch.empty(kara.workspace_size(params, nt, L), dtype=torch.uint8, device=dev)
     scores = torch.empty((L, nt, H, N), dtype=torch.float32, device=dev)
     disc = torch.empty((L, nt, H, p["budget"] - p["chunk_budget"]), dtype=torch.int32, device=dev)
@@ -95,18 +103,25 @@ def test_fullsize_sampled(name, n_p1, n_p2):
     assert (st == 0).all(), st
     print("[case] step done; checking", flush=True)
 
-    # P2 on a larger sample: the oracle's selection on the GPU's own scores
-    p2_units = _units_sample(rng, L, nt, H, n_p2, corners=False)
-    sc_h, disc_h, kept_h = {}, {}, {}
-    idx = torch.tensor(p2_units + p1_units, dtype=torch.int64)
-    sc_sel = scores[idx[:, 0], idx[:, 1], idx[:, 2]].cpu().numpy()
-    di_sel = disc[idx[:, 0], idx[:, 1], idx[:, 2]].cpu().numpy()
-    ke_sel = kept[idx[:, 0], idx[:, 1], idx[:, 2]].cpu().numpy()
-    for i, u in enumerate(p2_units + p1_units):
-        sc_h[u], disc_h[u], kept_h[u] = sc_sel[i], di_sel[i], ke_sel[i]
-        d, k = oracle.kept_set(sc_h[u], p["budget"], p["chunk_budget"], p["max_chunk_len"])
-        assert np.array_equal(d, disc_h[u]), f"P2 discrete at {u}"
-        assert np.array_equal(k, kept_h[u]), f"P2 kept at {u}"
+    # P2 on every unit: the oracle's selection on the GPU's own scores
+    sc_all, di_all, ke_all = scores.cpu().numpy(), disc.cpu().numpy(), kept.cpu().numpy()
+    n_units = 0
+    for l in range(L):
+        for t in range(nt):
+            for h in range(H):
+                d, k = oracle.kept_set(sc_all[l, t, h], p["budget"], p["chunk_budget"], p["max_chunk_len"])
+                assert np.array_equal(d, di_all[l, t, h]), f"P2 discrete at {(l, t, h)}"
+                assert np.array_equal(k, ke_all[l, t, h]), f"P2 kept at {(l, t, h)}"
+                n_units += 1
+        if l % 10 == 9:
+            print(f"[case] P2 through layer {l}", flush=True)
+    sc_h, kept_h = {}, {}
+    for u in p1_units:
+        sc_h[u], kept_h[u] = sc_all[u], ke_all[u]
+
+    # compaction of every unit against its definition, on the device
+    snap.check(geom, p, kept, kp, vp)
+    del snap
 
     # P1 and P3 on the sampled units (fp64 scores from the host copies)
     scale = oracle.scale_of(p)
@@ -155,7 +170,7 @@ def test_fullsize_sampled(name, n_p1, n_p2):
             got = _rows(pool, bt_h[s], np.arange(new), h, bs)
             assert want.shape == got.shape
             assert np.array_equal(want.view(np.uint8), got.view(np.uint8)), f"P4 {name_} rows of {u}"
-    print(f"[case] ok: P1 max rel err {worst:.2e} over {len(p1_units)} units, P2 over {len(sc_h)} units, "
+    print(f"[case] ok: P1 max rel err {worst:.2e} over {len(p1_units)} units, P2 and compaction over {n_units} units, "
           f"P3 near-tie differences {differ}", flush=True)
     del q, kp, vp, ws, scores, disc, kept
     torch.cuda.empty_cache()

@@ -153,3 +153,69 @@ def test_validation_flags_and_leaves_flagged_untouched():
     np.testing.assert_array_equal(pool, before)
     np.testing.assert_array_equal(table, tb)
     assert list(seq_lens) == [13, 13, 13, 5]
+
+
+def test_device_compaction_checker_on_the_oracle():
+    """The all-units compaction check of the full-size GPU test, run on the
+    CPU: it accepts the oracle's compaction and rejects a swapped row, a row
+    of the wrong head and a changed row before the window."""
+    torch = pytest.importorskip("torch")
+    import kara_check as kc
+    import kara_inputs as ki
+
+    cfg = ki.workload("batch8", n_seqs=3, n_layers=2, buffer=32, budget=199, prefix=(40, 300), tail=(0, 15),
+                      num_pages=512)
+    geom = ki.make_geometry(cfg)
+    p = geom.params()
+    L, nt, H, bs = cfg["n_layers"], len(geom.trig), p["n_kv_heads"], p["block_size"]
+    W, U, N = p["window"], p["buffer"], p["window"] - p["buffer"]
+    kp, vp = zip(*(ki.make_pools(geom, l, "cpu") for l in range(L)))
+    kp, vp = list(kp), list(vp)
+    # rows before the window carry data too, so that a write there shows
+    for pools in (kp, vp):
+        for pool in pools:
+            pool.add_(torch.randn(pool.shape, generator=torch.Generator().manual_seed(5)).to(pool.dtype))
+    snap = kc.WindowSnapshot(geom, kp, vp)
+
+    rng = np.random.default_rng(3)
+    kept = np.zeros((L, nt, H, p["budget"]), dtype=np.int32)
+    for l in range(L):
+        for t, s in enumerate(geom.trig):
+            p0, old = int(geom.win_start[s]), int(geom.seq_lens[s])
+            pos = np.arange(p0, old)
+            pg, sl = geom.block_table[s, pos // bs], pos % bs
+            for h in range(H):
+                a = rng.random(N).astype(np.float32)
+                _, kept[l, t, h] = oracle.kept_set(a, p["budget"], p["chunk_budget"], p["max_chunk_len"])
+                for pool in (kp[l], vp[l]):
+                    rows = pool[pg, h, sl, :].view(torch.int16).numpy()     # raw bf16 bits
+                    moved = oracle.gather_rows(rows, kept[l, t, h], W, U)
+                    pool[pg[:len(moved)], h, sl[:len(moved)], :] = torch.from_numpy(moved).view(torch.bfloat16)
+    kept_t = torch.from_numpy(kept)
+    snap.check(geom, p, kept_t, kp, vp)
+
+    s0 = int(geom.trig[1])
+    p0 = int(geom.win_start[s0])
+    page, slot = lambda x: int(geom.block_table[s0, x // bs]), lambda x: x % bs
+
+    # a swapped pair of kept rows (layer 1, head 0, destinations 3 and 4)
+    a_, b_ = p0 + 3, p0 + 4
+    ra, rb = vp[1][page(a_), 0, slot(a_)].clone(), vp[1][page(b_), 0, slot(b_)].clone()
+    vp[1][page(a_), 0, slot(a_)], vp[1][page(b_), 0, slot(b_)] = rb, ra
+    with pytest.raises(AssertionError, match="V kept rows of layer 1"):
+        snap.check(geom, p, kept_t, kp, vp)
+    vp[1][page(a_), 0, slot(a_)], vp[1][page(b_), 0, slot(b_)] = ra, rb
+
+    # a buffer row taken from the neighbouring head
+    d_ = p0 + p["budget"] + 2
+    r0 = kp[0][page(d_), 1, slot(d_)].clone()
+    kp[0][page(d_), 1, slot(d_)] = kp[0][page(d_), 0, slot(d_)]
+    with pytest.raises(AssertionError, match="K buffer/tail rows of layer 0"):
+        snap.check(geom, p, kept_t, kp, vp)
+    kp[0][page(d_), 1, slot(d_)] = r0
+
+    # a row before the window overwritten
+    x = p0 - 1
+    kp[1][page(x), 2, slot(x), 5] += 1
+    with pytest.raises(AssertionError, match="rows before the window, layer 1"):
+        snap.check(geom, p, kept_t, kp, vp)
