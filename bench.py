@@ -498,21 +498,6 @@ def run_recompute(args):
         meta["bt"].copy_(meta["bt0"], non_blocking=True)
         meta["seq_lens"].copy_(meta["seq_lens0"], non_blocking=True)
 
-    # Device backup of the rows compaction overwrites, taken before any step:
-    # each staged pass below starts from the same pools (restored outside
-    # its events), so every pass compresses the same input.  The timed steps
-    # run back to back on the pools the previous step left; scoring and
-    # selection cost does not depend on that, and compaction skips the kept
-    # rows that are already in place.
-    pg, sl = (torch.from_numpy(a).to(device) for a in dest_rows(geom, p, nw))
-    backup = [(k[pg, :, sl, :], v[pg, :, sl, :]) for k, v in zip(kp, vp)]
-    log(f"pool backup: {len(pg)} rows per layer, {sum(b.numel() * b.element_size() for kv in backup for b in kv) / 1e9:.2f} GB")
-
-    def restore_pools():
-        for (bk, bv), k, v in zip(backup, kp, vp):
-            k[pg, :, sl, :] = bk
-            v[pg, :, sl, :] = bv
-
     def event(evs=None):
         restore()
         if evs:

@@ -3,11 +3,15 @@
 // triggered sequence, at cache position p0 + w, attends to cache rows
 // [0, p0 + w]; query head hq reads KV head hq / G.
 //
-// One workgroup of 4 waves owns 16*QT*4 query rows of one (sequence, KV
+// One workgroup of 8 waves owns 16*QT*8 query rows of one (sequence, KV
 // head), rows ordered (window position, head in group), and streams the
-// cache rows [0, p0 + last row's position] through LDS in 64-key chunks,
-// double buffered: K as stored ([key][d], 16-byte chunks XOR-swizzled by
-// row) and V transposed ([d][key], 8-byte units XOR-swizzled by row).
+// cache rows [0, p0 + last row's position] through a four-stage LDS ring in
+// 64-key chunks, three chunks ahead of the one being worked on: K and V as
+// stored ([key][d], 16-byte chunks XOR-swizzled by row; V is read through
+// the transposed LDS load).  The pages of the rows come from a copy of the
+// sequence's block-table row in LDS, so inside the chunk loop the only
+// global memory operations are the copies, and the wait for a chunk counts
+// exactly the copies issued after it.
 //
 // Per chunk and 16-query tile a wave forms S^T = K Q^T with
 // v_mfma_f32_16x16x32_bf16 (keys as the M dimension), so a lane holds four
@@ -32,9 +36,11 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-constexpr int kAttnThreads = 256;
+constexpr int kAttnThreads = 512;
 constexpr int kAttnWaves = kAttnThreads / 64;
 constexpr int kKeys = 64;                   // keys per chunk
+constexpr int kStages = 4;                  // LDS ring: chunks ch .. ch+3 resident or in flight
+constexpr int kPageTbl = 2048;              // block-table entries held in LDS at a time
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kMaxFloor = -1e30f;         // finite start of a running maximum
@@ -51,9 +57,10 @@ struct ACfg {
   static constexpr int kRowsWG = kAttnWaves * kRowsWave;
   static constexpr int kKBytes = kKeys * kRowBytes;    // one chunk of K (or V) rows
   static constexpr int kStage = 2 * kKBytes;           // K rows, then V rows
-  static constexpr int kStages = 2;
   static constexpr int kCopies = kKBytes / (kAttnThreads * 16);      // 16-byte copies per thread per pool
+  static constexpr int kPerChunk = 2 * kCopies;        // copy instructions per thread per chunk
   static_assert(kCopies * kAttnThreads * 16 == kKBytes, "uniform copies");
+  static_assert(kStages * kStage + kPageTbl * 4 <= 160 * 1024, "LDS budget");
 };
 
 struct AttnArgs {
@@ -98,7 +105,25 @@ __device__ inline void copy16(const void* g, char* lds_wave_base) {
 
 // Barrier for LDS traffic only (the copies it covers are waited for first).
 __device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
-__device__ inline void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+template <int N>
+__device__ inline void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Wait for this thread's copies of a chunk when the copies of `newer` later
+// chunks (0 .. kStages-2, run-time) were issued after them.
+template <int kPerChunk>
+__device__ inline void wait_chunk(int newer) {
+  static_assert(kStages == 4, "wait_chunk covers up to two newer chunks");
+  if (newer >= 2) {
+    wait_vm<2 * kPerChunk>();
+  } else if (newer == 1) {
+    wait_vm<kPerChunk>();
+  } else {
+    wait_vm<0>();
+  }
+}
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 
@@ -110,12 +135,11 @@ __device__ inline v4i16 read_tr(const char* p) {
 }
 
 template <int D, int QT>
-__global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(AttnArgs a) {
+__global__ __launch_bounds__(kAttnThreads, 1) void attn_kernel(AttnArgs a) {
   using C = ACfg<D, QT>;
-  __shared__ __attribute__((aligned(16))) char smem[C::kStages * C::kStage];
-  // 16-byte-unit offsets of a chunk's 64 cache rows inside a pool (K and V
-  // pools share the layout); three chunks: issuing, next, being filled
-  __shared__ uint32_t row_off[3][kKeys];
+  __shared__ __attribute__((aligned(16))) char smem[kStages * C::kStage];
+  // pages of the sequence's logical blocks [pt_base, pt_base + kPageTbl)
+  __shared__ int32_t ptbl[kPageTbl];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -173,17 +197,19 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(AttnArgs a) {
     for (int dt = 0; dt < C::kDT; ++dt) o[qt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // ---- row offsets (wave 0, one lane per row) and copies ----
-  // rows past kend repeat row kend - 1: finite, and masked for every query
-  auto page_of = [&](int ch) -> int {
-    const int pos = min(ch * kKeys + lane, kend - 1);
-    return row_pages[pos / a.bs];
+  // ---- block-table segment in LDS, and copies ----
+  // Chunk ch's rows are positions ch*64 .. ch*64+63 (past kend: row kend-1,
+  // finite and masked for every query).  A chunk never straddles two
+  // segments: a segment spans kPageTbl*bs positions, a multiple of 64.
+  const int seg_pos = kPageTbl * a.bs;
+  const int n_blk = (kend + a.bs - 1) / a.bs;
+  int pt_base = -1;                      // first block held in ptbl (uniform)
+  auto load_segment = [&](int seg) __attribute__((always_inline)) {
+    pt_base = seg * kPageTbl;
+    const int n = min(kPageTbl, n_blk - pt_base);
+    for (int i = tid; i < n; i += kAttnThreads) ptbl[i] = row_pages[pt_base + i];
   };
-  auto put_offset = [&](int ch, int page) {
-    const int pos = min(ch * kKeys + lane, kend - 1);
-    row_off[ch % 3][lane] = (uint32_t)((((int64_t)page * a.Hkv + h) * a.bs + pos % a.bs) * C::kCPR);
-  };
-  // copy r of this thread fills slot r*256 + tid of the K (V) region: row
+  // copy r of this thread fills slot r*512 + tid of the K (V) region: row
   // kr = slot / kCPR, stored chunk slot % kCPR, fetched chunk (slot % kCPR) ^ (kr & kSwz)
   int kr_of[C::kCopies], chunk_of[C::kCopies];
 #pragma unroll
@@ -193,21 +219,28 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(AttnArgs a) {
     chunk_of[r] = (slot % C::kCPR) ^ (kr_of[r] & C::kSwz);
   }
   auto issue = [&](int ch) __attribute__((always_inline)) {
-    char* st = smem + (ch % C::kStages) * C::kStage;
+    if (ch * kKeys >= (pt_base + kPageTbl) * a.bs) {
+      // next segment (rare): every earlier copy lands first, as the table's
+      // loads are waited for with the compiler's own count
+      wait_vm<0>();
+      lds_barrier();
+      load_segment(ch * kKeys / seg_pos);
+      lds_barrier();
+    }
+    char* st = smem + (ch % kStages) * C::kStage;
 #pragma unroll
     for (int r = 0; r < C::kCopies; ++r) {
-      const uint64_t off = (uint64_t)row_off[ch % 3][kr_of[r]] * 16 + chunk_of[r] * 16;
+      const int pos = min(ch * kKeys + kr_of[r], kend - 1);
+      const int page = ptbl[pos / a.bs - pt_base];
+      const uint64_t off = ((((uint64_t)page * a.Hkv + h) * a.bs + pos % a.bs) * C::kCPR + chunk_of[r]) * 16;
       copy16(a.kpool + off, st + (r * kAttnWaves + wave) * 1024);
       copy16(a.vpool + off, st + C::kKBytes + (r * kAttnWaves + wave) * 1024);
     }
   };
 
-  if (wave == 0) {
-    put_offset(0, page_of(0));
-    if (n_chunks > 1) put_offset(1, page_of(1));
-  }
+  load_segment(0);
   lds_barrier();
-  issue(0);
+  for (int c = 0; c < kStages - 1 && c < n_chunks; ++c) issue(c);
 
   // Per-lane LDS byte offsets of the operand reads.  K operand rows are
   // 16*kt + li, so row & kSwz = li & kSwz and the swizzled chunk depends on
@@ -315,14 +348,13 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attn_kernel(AttnArgs a) {
   // first chunk in which some key lies past its first row.  Two loops over
   // the same step keep the unmasked code free of the mask.
   auto step = [&](int ch, auto masked) __attribute__((always_inline)) {
-    wait_copies();
+    // chunks ch+1 .. ch+kStages-2 were issued after chunk ch
+    wait_chunk<C::kPerChunk>(min(kStages - 2, n_chunks - 1 - ch));
     lds_barrier();
-    if (ch + 1 < n_chunks) issue(ch + 1);
-    int next_page = 0;
-    if (wave == 0 && ch + 2 < n_chunks) next_page = page_of(ch + 2);
+    // the stage of chunk ch-1 is free: every wave has passed this barrier
+    if (ch + kStages - 1 < n_chunks) issue(ch + kStages - 1);
     const int k0 = ch * kKeys;
-    if (k0 <= wave_last_pos) chunk_work(smem + (ch % C::kStages) * C::kStage, k0, masked);
-    if (wave == 0 && ch + 2 < n_chunks) put_offset(ch + 2, next_page);
+    if (k0 <= wave_last_pos) chunk_work(smem + (ch % kStages) * C::kStage, k0, masked);
   };
   // first chunk whose last key passes this wave's first row position
   const int first_masked = min(n_chunks, wave_first_pos >= kKeys - 1 ? (wave_first_pos - (kKeys - 1)) / kKeys + 1 : 0);

@@ -86,6 +86,8 @@ def _oracle_attention(geom, p, q_h, kp_h, vp_h, t, rows=None):
     (96, 40, 8, 128, 7, (10, 130)),        # G = 5 (Qwen3-14B), unaligned blocks
     (128, 4, 4, 64, 16, (0, 100)),         # G = 1, d = 64
     (256, 32, 8, 128, 256, (0, 600)),      # serving geometry: 256-token blocks
+    (64, 8, 2, 128, 1, (2050, 2400)),      # one-token blocks past 2048: a second block-table segment
+    (80, 8, 2, 64, 2, (4050, 4500)),       # d = 64, two-token blocks past 4096: the same switch
 ])
 def test_attention_parity(window, n_q, n_kv, d, bs, prefix):
     from paper_2607_01237_amd import kara
