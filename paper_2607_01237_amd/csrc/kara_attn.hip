@@ -19,7 +19,8 @@
 // chunk, and the probabilities, converted to bf16, are already the B
 // operand of O^T += V^T P^T (the k index of that product runs over keys in
 // the order the S^T tiles left them; V^T is read in the same order).  The
-// row sums stay per lane until the end.  The softmax reference maximum is
+// row sums come from the same product with an all-ones A operand, so the
+// normalisation uses exactly the bf16 weights the numerator used.  The softmax reference maximum is
 // raised lazily (only past a headroom of 2^8), which skips the rescaling of
 // the accumulators on almost every chunk.  Exponentials are the bare
 // v_exp_f32: arguments below the normal range flush to 0, which is the
@@ -40,6 +41,7 @@ constexpr int kAttnThreads = 512;
 constexpr int kAttnWaves = kAttnThreads / 64;
 constexpr int kKeys = 64;                   // keys per chunk
 constexpr int kStages = 4;                  // LDS ring: chunks ch .. ch+3 resident or in flight
+constexpr int kLookahead = kStages - 1;     // chunks copied ahead of the one being worked on
 constexpr int kPageTbl = 2048;              // block-table entries held in LDS at a time
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kNegInf = -__builtin_huge_valf();
@@ -50,7 +52,20 @@ template <int D, int QT>
 struct ACfg {
   static constexpr int kRowBytes = D * 2;
   static constexpr int kCPR = kRowBytes / 16;          // 16-byte chunks per row
-  static constexpr int kSwz = kCPR - 1;                // XOR swizzle of chunks by row
+  static constexpr int kSwz = kCPR - 1;
+  // XOR swizzles of a row's 16-byte chunks.  K (read 16 rows x 16 bytes per
+  // lane group): by the row, its two 2-bit halves swapped at d = 128.  V
+  // (read through the transposed load, 32 lanes x 8 bytes at a time over 8
+  // rows and two adjacent chunks): by twice the row (twice its half at
+  // d = 64, whose rows are half a bank sweep), so the 16 (row, chunk) pairs
+  // of such a read land in 16 distinct chunks.  Both measured on gfx950
+  // (d = 128) free of bank conflicts; XOR by the row itself costs about four
+  // conflict cycles per K read and two per V read.
+  static __device__ __forceinline__ int swz_k(int row) {
+    if constexpr (D == 128) return ((row & 3) << 2) | ((row >> 2) & 3);
+    return row & kSwz;
+  }
+  static __device__ __forceinline__ int swz_v(int row) { return (2 * (D == 128 ? row : row >> 1)) & kSwz; }
   static constexpr int kKS = kCPR / 4;                 // k-steps of one dot product (per lane group)
   static constexpr int kDT = D / 16;                   // 16-row tiles of O^T
   static constexpr int kRowsWave = 16 * QT;
@@ -65,6 +80,7 @@ struct ACfg {
 
 struct AttnArgs {
   int W, Hq, Hkv, G, bs, max_blocks, n_trig;
+  int bs_shift;               // log2(bs) when bs is a power of two, else -1
   float c;                    // logit scale times log2(e)
   const char* q;              // [n_trig][W][Hq][d]
   const char* kpool;          // [pages][Hkv][bs][d]
@@ -115,7 +131,7 @@ __device__ inline void wait_vm() {
 // chunks (0 .. kStages-2, run-time) were issued after them.
 template <int kPerChunk>
 __device__ inline void wait_chunk(int newer) {
-  static_assert(kStages == 4, "wait_chunk covers up to two newer chunks");
+  static_assert(kLookahead == 3, "wait_chunk covers up to two newer chunks");
   if (newer >= 2) {
     wait_vm<2 * kPerChunk>();
   } else if (newer == 1) {
@@ -138,8 +154,9 @@ template <int D, int QT>
 __global__ __launch_bounds__(kAttnThreads, 1) void attn_kernel(AttnArgs a) {
   using C = ACfg<D, QT>;
   __shared__ __attribute__((aligned(16))) char smem[kStages * C::kStage];
-  // pages of the sequence's logical blocks [pt_base, pt_base + kPageTbl)
-  __shared__ int32_t ptbl[kPageTbl];
+  // row index (page*Hkv + h)*bs of slot 0 of the sequence's logical blocks
+  // [pt_base, pt_base + kPageTbl), for this workgroup's KV head
+  __shared__ uint32_t ptbl[kPageTbl];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -187,15 +204,21 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_kernel(AttnArgs a) {
   const int wave_first_pos = p0 + min(wrow0, R - 1) / a.G;
   const int wave_last_pos = p0 + min(wrow0 + C::kRowsWave - 1, R - 1) / a.G;
 
-  floatx4 o[QT][C::kDT];
-  float m[QT], l[QT];
+  // o: O^T tiles; l: the row sums, formed on the matrix cores as one more
+  // 16-row tile whose A operand is all ones (every lane then holds its
+  // query's sum of the bf16 weights PV used, four times)
+  floatx4 o[QT][C::kDT], l[QT];
+  float m[QT];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     m[qt] = kMaxFloor;
-    l[qt] = 0.f;
+    l[qt] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int dt = 0; dt < C::kDT; ++dt) o[qt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
   }
+  bf16x8 ones;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) ones[i] = (__bf16)1.f;
 
   // ---- block-table segment in LDS, and copies ----
   // Chunk ch's rows are positions ch*64 .. ch*64+63 (past kend: row kend-1,
@@ -207,16 +230,19 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_kernel(AttnArgs a) {
   auto load_segment = [&](int seg) __attribute__((always_inline)) {
     pt_base = seg * kPageTbl;
     const int n = min(kPageTbl, n_blk - pt_base);
-    for (int i = tid; i < n; i += kAttnThreads) ptbl[i] = row_pages[pt_base + i];
+    for (int i = tid; i < n; i += kAttnThreads)
+      ptbl[i] = (uint32_t)(((int64_t)row_pages[pt_base + i] * a.Hkv + h) * a.bs);
   };
   // copy r of this thread fills slot r*512 + tid of the K (V) region: row
-  // kr = slot / kCPR, stored chunk slot % kCPR, fetched chunk (slot % kCPR) ^ (kr & kSwz)
-  int kr_of[C::kCopies], chunk_of[C::kCopies];
+  // kr = slot / kCPR, stored chunk slot % kCPR, fetched chunk (slot % kCPR)
+  // ^ swz(kr)
+  int kr_of[C::kCopies], chunk_k[C::kCopies], chunk_v[C::kCopies];
 #pragma unroll
   for (int r = 0; r < C::kCopies; ++r) {
     const int slot = r * kAttnThreads + tid;
     kr_of[r] = slot / C::kCPR;
-    chunk_of[r] = (slot % C::kCPR) ^ (kr_of[r] & C::kSwz);
+    chunk_k[r] = (slot % C::kCPR) ^ C::swz_k(kr_of[r]);
+    chunk_v[r] = (slot % C::kCPR) ^ C::swz_v(kr_of[r]);
   }
   auto issue = [&](int ch) __attribute__((always_inline)) {
     if (ch * kKeys >= (pt_base + kPageTbl) * a.bs) {
@@ -231,40 +257,49 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_kernel(AttnArgs a) {
 #pragma unroll
     for (int r = 0; r < C::kCopies; ++r) {
       const int pos = min(ch * kKeys + kr_of[r], kend - 1);
-      const int page = ptbl[pos / a.bs - pt_base];
-      const uint64_t off = ((((uint64_t)page * a.Hkv + h) * a.bs + pos % a.bs) * C::kCPR + chunk_of[r]) * 16;
-      copy16(a.kpool + off, st + (r * kAttnWaves + wave) * 1024);
-      copy16(a.vpool + off, st + C::kKBytes + (r * kAttnWaves + wave) * 1024);
+      int blk, slot;
+      if (a.bs_shift >= 0) {
+        blk = pos >> a.bs_shift;
+        slot = pos & (a.bs - 1);
+      } else {
+        blk = pos / a.bs;
+        slot = pos - blk * a.bs;
+      }
+      const uint64_t row = (uint64_t)(ptbl[blk - pt_base] + (uint32_t)slot) * C::kCPR;
+      copy16(a.kpool + (row + chunk_k[r]) * 16, st + (r * kAttnWaves + wave) * 1024);
+      copy16(a.vpool + (row + chunk_v[r]) * 16, st + C::kKBytes + (r * kAttnWaves + wave) * 1024);
     }
   };
 
   load_segment(0);
   lds_barrier();
-  for (int c = 0; c < kStages - 1 && c < n_chunks; ++c) issue(c);
+  for (int c = 0; c < kLookahead && c < n_chunks; ++c) issue(c);
 
   // Per-lane LDS byte offsets of the operand reads.  K operand rows are
-  // 16*kt + li, so row & kSwz = li & kSwz and the swizzled chunk depends on
+  // 16*kt + li, so swz_k(row) = swz_k(li) and the swizzled chunk depends on
   // the lane and ks only; V rows read through the transposed load are
-  // 32*j + 16*half + 4*gq + (li >> 2), whose low four bits do not depend on
-  // j or half.  The tile and half offsets are then compile-time constants.
+  // 32*j + 16*half + 4*gq + (li >> 2), and swz_v of such a row does not
+  // depend on j or half.  The tile and half offsets are then compile-time
+  // constants.
   int koff[C::kKS], voff[C::kDT];
 #pragma unroll
   for (int ks = 0; ks < C::kKS; ++ks)
-    koff[ks] = li * C::kRowBytes + (((gq * C::kKS + ks) ^ (li & C::kSwz)) * 16);
+    koff[ks] = li * C::kRowBytes + (((gq * C::kKS + ks) ^ C::swz_k(li)) * 16);
   {
     const int vrow = 4 * gq + (li >> 2);
 #pragma unroll
     for (int dt = 0; dt < C::kDT; ++dt)
-      voff[dt] = C::kKBytes + vrow * C::kRowBytes + (((dt * 2 + ((li & 3) >> 1)) ^ (vrow & C::kSwz)) * 16) +
+      voff[dt] = C::kKBytes + vrow * C::kRowBytes + (((dt * 2 + ((li & 3) >> 1)) ^ C::swz_v(vrow)) * 16) +
                  (li & 1) * 8;
   }
 
-  // One chunk of this wave's work; `masked` (a compile-time tag) selects
-  // the copy with the causal mask, used only where some key of the chunk
-  // lies past some row of the wave.
-  auto chunk_work = [&](const char* st, int k0, auto masked) __attribute__((always_inline)) {
-      // S^T tiles: keys kt*16 + (4*gq + r), query li
-      floatx4 sv[QT][4];
+  // One chunk of this wave's work in two phases: A forms the S^T tiles
+  // (`masked`, a compile-time tag, selects the copy with the causal mask,
+  // used only where some key of the chunk lies past some row of the wave),
+  // B does the online softmax and O^T += V^T P^T.
+  // S^T tiles: keys kt*16 + (4*gq + r), query li
+  floatx4 sv[QT][4];
+  auto phase_a = [&](const char* st, int k0, auto masked) __attribute__((always_inline)) {
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
 #pragma unroll
@@ -290,6 +325,8 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_kernel(AttnArgs a) {
             for (int r = 0; r < 4; ++r)
               if (k0 + kt * 16 + 4 * gq + r > qpos[qt]) sv[qt][kt][r] = kNegInf;
       }
+  };
+  auto phase_b = [&](const char* st) __attribute__((always_inline)) {
       // online softmax per query (lane's query li of each tile), in log2 units
       bf16x8 pb[QT][2];
 #pragma unroll
@@ -312,16 +349,11 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_kernel(AttnArgs a) {
           for (int dt = 0; dt < C::kDT; ++dt) o[qt][dt] *= alpha;
         }
         const float mr = m[qt];
-        float lsum = 0.f;
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float p = __builtin_amdgcn_exp2f(fmaf(sv[qt][kt][r], a.c, -mr));
-            lsum += p;
-            pb[qt][kt >> 1][(kt & 1) * 4 + r] = (__bf16)p;
-          }
-        l[qt] += lsum;
+          for (int r = 0; r < 4; ++r)
+            pb[qt][kt >> 1][(kt & 1) * 4 + r] = (__bf16)__builtin_amdgcn_exp2f(fmaf(sv[qt][kt][r], a.c, -mr));
       }
       // O^T += V^T P^T over two 32-key halves; lane (gq, li) reads, through
       // the transposed load, keys 32j + 4gq + (li >> 2) (+16) at head-dim
@@ -340,21 +372,30 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_kernel(AttnArgs a) {
           for (int qt = 0; qt < QT; ++qt)
             o[qt][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[qt][j], o[qt][dt], 0, 0, 0);
         }
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) l[qt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pb[qt][j], l[qt], 0, 0, 0);
       }
   };
 
   // Every wave passes the same barriers chunk by chunk; a wave works on the
   // chunks up to its last row's position, with the causal mask from the
   // first chunk in which some key lies past its first row.  Two loops over
-  // the same step keep the unmasked code free of the mask.
+  // the same step keep the unmasked code free of the mask.  (Staggering the
+  // two waves of each SIMD half a chunk apart, as the scoring kernel does,
+  // was measured slower here: the lagging waves keep chunk ch-1's stage in
+  // use, which leaves room for two chunks of lookahead instead of three.)
   auto step = [&](int ch, auto masked) __attribute__((always_inline)) {
-    // chunks ch+1 .. ch+kStages-2 were issued after chunk ch
-    wait_chunk<C::kPerChunk>(min(kStages - 2, n_chunks - 1 - ch));
+    // chunks ch+1 .. ch+kLookahead-1 were issued after chunk ch
+    wait_chunk<C::kPerChunk>(min(kLookahead - 1, n_chunks - 1 - ch));
     lds_barrier();
     // the stage of chunk ch-1 is free: every wave has passed this barrier
-    if (ch + kStages - 1 < n_chunks) issue(ch + kStages - 1);
+    if (ch + kLookahead < n_chunks) issue(ch + kLookahead);
     const int k0 = ch * kKeys;
-    if (k0 <= wave_last_pos) chunk_work(smem + (ch % kStages) * C::kStage, k0, masked);
+    if (k0 <= wave_last_pos) {
+      const char* st = smem + (ch % kStages) * C::kStage;
+      phase_a(st, k0, masked);
+      phase_b(st);
+    }
   };
   // first chunk whose last key passes this wave's first row position
   const int first_masked = min(n_chunks, wave_first_pos >= kKeys - 1 ? (wave_first_pos - (kKeys - 1)) / kKeys + 1 : 0);
@@ -365,9 +406,7 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_kernel(AttnArgs a) {
   // ---- normalise and store: lane holds O^T[dt*16 + 4*gq + r][query li] ----
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
-    float lt = l[qt] + __shfl_xor(l[qt], 16, 64);
-    lt += __shfl_xor(lt, 32, 64);
-    const float inv = 1.f / lt;
+    const float inv = 1.f / l[qt][0];
     const int r = wrow0 + qt * 16 + li;
     if (r >= R) continue;
     const int w = r / a.G;
@@ -452,6 +491,7 @@ hipError_t launch_recompute_attention(const Geom& g, const void* q, const void* 
   a.bs = g.bs;
   a.max_blocks = g.max_blocks;
   a.n_trig = g.n_trig;
+  a.bs_shift = (g.bs & (g.bs - 1)) == 0 ? __builtin_ctz((unsigned)g.bs) : -1;
   a.c = g.scale * kLog2e;
   a.q = (const char*)q;
   a.kpool = (const char*)k_pool;

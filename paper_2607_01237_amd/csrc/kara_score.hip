@@ -72,6 +72,15 @@ struct Cfg {
   static constexpr int kRowBytes = D * kES;              // one key or query row
   static constexpr int kCPR = kRowBytes / 16;            // 16-byte chunks per row
   static constexpr int kSwz = kCPR < 16 ? kCPR - 1 : 15; // XOR swizzle mask
+  // XOR swizzle of a key row's 16-byte chunks, a function of the row.  For
+  // 256-byte rows (bf16, d = 128) the row's two 2-bit halves are swapped
+  // first: measured on gfx950, a 16-byte read of 16 rows x 4 lane groups then
+  // has no bank conflicts, where XOR by the row itself costs about four
+  // conflict cycles per read.
+  static __device__ __forceinline__ int swz(int row) {
+    if constexpr (kCPR == 16) return ((row & 3) << 2) | ((row >> 2) & 3);
+    return row & kSwz;
+  }
   static constexpr int kRowsWG = kScoreWaves * 16 * RT;  // query rows per workgroup
   static constexpr int kStageBytes = kChunkKeys * kRowBytes;
   static constexpr int kL = kStageBytes / (kScoreThreads * 16);   // copies per thread per chunk
@@ -275,7 +284,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
 
   // ---- key copies: every thread issues exactly kL per chunk ----
   // Copy r of this thread fills stage slot r*512 + tid: key row kr = slot /
-  // CPR of the chunk, 16-byte chunk (slot % CPR) ^ (kr & kSwz).  The key
+  // CPR of the chunk, 16-byte chunk (slot % CPR) ^ swz(kr).  The key
   // offsets of a chunk are read from the table one iteration before its
   // copies are issued, so issuing them never waits on LDS.
   const char* kpool_c[kL];
@@ -284,7 +293,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
   for (int r = 0; r < kL; ++r) {
     const int slot = r * kScoreThreads + tid;
     const int kr = slot / CPR;
-    const int chunk = (slot % CPR) ^ (kr & C::kSwz);
+    const int chunk = (slot % CPR) ^ C::swz(kr);
     kpool_c[r] = kpool + chunk * 16;
     kr0[r] = kr;
   }
@@ -306,7 +315,7 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
   // multiples of 16 plus li, so the swizzle term depends on the lane only)
   int koff[KC];
 #pragma unroll
-  for (int ks = 0; ks < KC; ++ks) koff[ks] = li * C::kRowBytes + (((gq * KC + ks) ^ (li & C::kSwz)) * 16);
+  for (int ks = 0; ks < KC; ++ks) koff[ks] = li * C::kRowBytes + (((gq * KC + ks) ^ C::swz(li)) * 16);
 
   // logits of this wave's rows x the chunk's 64 keys:
   // acc[rt][ti][q] = row rt*16 + 4*gq + q, key ti*16 + li
