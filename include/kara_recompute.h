@@ -28,11 +28,15 @@
  * with nothing enqueued, per-sequence problems in status[t] (KARA_SEQ_*):
  * index out of range, listed twice, window past the sequence end
  * (p0 + window > seq_len), or a page of [0, p0 + window) outside the pool.
- * A flagged sequence's outputs are left unwritten.  bf16 only
+ * A flagged sequence's attention output and scoring queries are left
+ * unwritten; kara_recompute_queries runs the matrix products over every
+ * listed row, so a flagged sequence's hidden_out rows are unspecified.  bf16 only
  * (params.dtype = KARA_BF16, else KARA_ERR_UNSUPPORTED), head_dim 64 or 128.
  * Device arrays are 16-byte aligned.  kara_recompute_queries creates one
  * rocBLAS handle per device on its first call there; rocBLAS allocates that
- * handle's own workspace.
+ * handle's own workspace.  Each call binds that handle to its stream, so
+ * calls on one device from several host threads at once must be serialised
+ * by the caller.
  *
  * Layouts (row-major)
  *   q, out (attention)  [n_trig][window][n_q_heads][head_dim] bf16

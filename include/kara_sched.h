@@ -63,6 +63,9 @@
  * KARA_ERR_INVALID_ARG.  kara_sched_event_commit returns
  * KARA_ERR_SCHED_MISMATCH when the device's freed list differs from the
  * host's; the host state is updated from its own computation either way.
+ * KARA_ERR_SCHED_NOMEM reports that host memory for the scheduler's tables
+ * or queues could not be allocated; the scheduler is then in an unspecified
+ * state and may only be destroyed.
  * Pointers returned in the step / event / tables structs point into the
  * scheduler and stay valid until the next call on it.  A scheduler must not
  * be used from two threads at once.
@@ -80,6 +83,8 @@ extern "C" {
 
 /* The device's freed-page list differs from the host's model of it. */
 #define KARA_ERR_SCHED_MISMATCH (-5)
+/* Host memory for the scheduler could not be allocated. */
+#define KARA_ERR_SCHED_NOMEM (-6)
 
 typedef struct kara_sched kara_sched_t;
 

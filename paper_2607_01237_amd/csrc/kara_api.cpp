@@ -205,6 +205,7 @@ const char* kara_status_string(int32_t s) {
     case KARA_ERR_WORKSPACE: return "KARA_ERR_WORKSPACE: workspace missing or too small";
     case KARA_ERR_HIP: return "KARA_ERR_HIP: the HIP runtime rejected a launch";
     case -5: return "KARA_ERR_SCHED_MISMATCH: the device's freed pages differ from the scheduler's";
+    case -6: return "KARA_ERR_SCHED_NOMEM: host memory for the scheduler could not be allocated";
     default: return "unknown kara status";
   }
 }

@@ -18,7 +18,7 @@ HEADERS = [os.path.join(os.path.dirname(_PKG), "include", h)
            for h in ("kara.h", "kara_harness.h", "kara_sched.h", "kara_recompute.h")]
 
 BF16, F32 = 0, 1
-OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_SCHED_MISMATCH = 0, -1, -2, -3, -4, -5
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_SCHED_MISMATCH, ERR_SCHED_NOMEM = 0, -1, -2, -3, -4, -5, -6
 SEQ_OK, SEQ_BAD_WINDOW, SEQ_BAD_PAGE, SEQ_DUP_TRIGGER, SEQ_BAD_INDEX, SEQ_BAD_KEPT = 0, 1, 2, 4, 8, 16
 MAX_COMPRESSIBLE = 4096
 REQ_WAITING, REQ_RUNNING, REQ_FINISHED = 0, 1, 2
