@@ -96,9 +96,17 @@ def test_null_pointers_rejected_before_launch(lib):
     assert lib.kara_score_window(r, 4, None, 1, None, None, None, None, None, None, None, None, 0, None) == kara.ERR_INVALID_ARG
     assert lib.kara_compress_window(r, 4, None, 1, None, None, None, None, None, None, 1, None, None, None, None,
                                     None, None, None, 0, None) == kara.ERR_INVALID_ARG
-    # nothing to do is not an error
+    # nothing to do is not an error, and touches no pointer
     assert lib.kara_select(r, 0, None, None, None) == kara.OK
     assert lib.kara_validate(r, 0, None, None, None, None, None, None) == kara.OK
+    assert lib.kara_token2chunk(r, 0, None, None, None, None) == kara.OK
+    assert lib.kara_commit_tables(r, 0, None, None, None, None, None, None, None, None) == kara.OK
+    assert lib.kara_compact_pages(r, 0, None, 1, None, None, None, None, None, None, None, None) == kara.OK
+    assert lib.kara_score_window(r, 0, None, 1, None, None, None, None, None, None, None, None, 0, None) == kara.OK
+    assert lib.kara_compress_window(r, 0, None, 1, None, None, None, None, None, None, 1, None, None, None, None,
+                                    None, None, None, 0, None) == kara.OK
+    assert lib.kara_compress_prefill(r, 0, None, 2, 1, None, None, None, None, None, None, 1, None, None, None,
+                                     None, None, None, None, 0, None) == kara.OK
 
 
 def test_workspace_checked_before_launch(lib):

@@ -106,6 +106,16 @@ def test_bf16_long_window():
     _run(cfg)
 
 
+@pytest.mark.parametrize("window,buffer", [(4096, 0), (4128, 32)])
+def test_maximum_compressible_window(window, buffer):
+    # N = 4096, the largest compressible length the library takes: 64 chunks
+    # of 64 keys in each scoring sweep, the 16-position selection instance
+    # at its limit; with a buffer, the buffer queries score as well
+    cfg = ki.workload("batch8", n_seqs=2, n_layers=1, n_q_heads=2, n_kv_heads=1, window=window, buffer=buffer,
+                      budget=820, prefix=(0, 100), tail=(0, 5), num_pages=1024, key_mode="normal")
+    _run(cfg)
+
+
 @pytest.mark.parametrize("pos,scale", [(700, 16.0), (300, 16.0), (40, 16.0), (700, -16.0)])
 def test_outlier_keys(pos, scale):
     # One window key per (sequence, head) scaled by 16 (exact in bf16).
