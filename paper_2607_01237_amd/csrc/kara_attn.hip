@@ -382,8 +382,8 @@ __global__ __launch_bounds__(kAttnThreads, 1) void attn_kernel(AttnArgs a) {
   // first chunk in which some key lies past its first row.  Two loops over
   // the same step keep the unmasked code free of the mask.  (Staggering the
   // two waves of each SIMD half a chunk apart, as the scoring kernel does,
-  // was measured slower here: the lagging waves keep chunk ch-1's stage in
-  // use, which leaves room for two chunks of lookahead instead of three.)
+  // was measured slower here, also with K and V in rings of their own that
+  // keep three chunks of lookahead.)
   auto step = [&](int ch, auto masked) __attribute__((always_inline)) {
     // chunks ch+1 .. ch+kLookahead-1 were issued after chunk ch
     wait_chunk<C::kPerChunk>(min(kLookahead - 1, n_chunks - 1 - ch));
