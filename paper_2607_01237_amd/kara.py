@@ -197,6 +197,55 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
+# ---- host-side shape checks: the library takes bare pointers and cannot
+# tell a short or mistyped tensor from a right one
+
+def _need(name, t, n, dtype=None):
+    """t (a GPU tensor, or None) holds at least n elements of dtype."""
+    if t is None:
+        return
+    if dtype is not None and t.dtype != dtype:
+        raise KaraError("marshal", ERR_INVALID_ARG, f"{name}: dtype {t.dtype}, expected {dtype}")
+    if t.numel() < n:
+        raise KaraError("marshal", ERR_INVALID_ARG, f"{name}: {t.numel()} elements, at least {n} needed")
+
+
+def _dt(p):
+    import torch
+    return torch.bfloat16 if p.dtype == BF16 else torch.float32
+
+
+def _i32():
+    import torch
+    return torch.int32
+
+
+def _f32():
+    import torch
+    return torch.float32
+
+
+def _tables(p, block_table, seq_lens, win_start=None):
+    _need("block_table", block_table, p.n_seqs * p.max_blocks_per_seq, _i32())
+    _need("seq_lens", seq_lens, p.n_seqs, _i32())
+    _need("win_start", win_start, p.n_seqs, _i32())
+
+
+def _pools(p, pools, name):
+    for i, t in enumerate(pools):
+        _need(f"{name}[{i}]", t, p.num_pages * p.n_kv_heads * p.block_size * p.head_dim, _dt(p))
+
+
+def _units(p, n_layers, n_trig, n_windows=1):
+    return n_layers * n_trig * n_windows * p.n_kv_heads
+
+
+def _step_outputs(p, units, scores, discrete, kept):
+    _need("scores", scores, units * (p.window - p.buffer), _f32())
+    _need("discrete", discrete, units * (p.budget - p.chunk_budget), _i32())
+    _need("kept", kept, units * p.budget, _i32())
+
+
 def _ptr_array(tensors):
     arr = (ctypes.c_void_p * len(tensors))()
     for i, t in enumerate(tensors):
@@ -221,12 +270,22 @@ def workspace_size(p: KaraParams, n_trig: int, n_layers: int) -> int:
 
 
 def validate(p, trig, block_table, seq_lens, win_start, status, stream=None):
+    _need("trig", trig, 0, _i32())
+    _need("status", status, trig.numel(), _i32())
+    _tables(p, block_table, seq_lens, win_start)
     _check("kara_validate", load().kara_validate(ctypes.byref(p), trig.numel(), _ptr(trig), _ptr(block_table),
                                                  _ptr(seq_lens), _ptr(win_start), _ptr(status), _stream(stream)))
 
 
 def score_window(p, trig, q, k_pools, block_table, seq_lens, win_start, scores, status, workspace,
                  stream=None):
+    nt, L = trig.numel(), len(k_pools)
+    _need("trig", trig, 0, _i32())
+    _need("q", q, L * nt * (p.score_queries or p.window) * p.n_q_heads * p.head_dim, _dt(p))
+    _pools(p, k_pools, "k_pools")
+    _tables(p, block_table, seq_lens, win_start)
+    _step_outputs(p, _units(p, L, nt), scores, None, None)
+    _need("status", status, nt, _i32())
     _check("kara_score_window", load().kara_score_window(
         ctypes.byref(p), trig.numel(), _ptr(trig), len(k_pools), _ptr(q), _ptr_array(k_pools),
         _ptr(block_table), _ptr(seq_lens), _ptr(win_start), _ptr(scores), _ptr(status),
@@ -235,30 +294,61 @@ def score_window(p, trig, q, k_pools, block_table, seq_lens, win_start, scores, 
 
 def select(p, scores, discrete, stream=None):
     n_units = scores.numel() // (p.window - p.buffer)
+    _step_outputs(p, n_units, scores, discrete, None)
     _check("kara_select", load().kara_select(ctypes.byref(p), n_units, _ptr(scores), _ptr(discrete),
                                              _stream(stream)))
 
 
 def token2chunk(p, scores, discrete, kept, stream=None):
     n_units = scores.numel() // (p.window - p.buffer)
+    _step_outputs(p, n_units, scores, discrete, kept)
     _check("kara_token2chunk", load().kara_token2chunk(ctypes.byref(p), n_units, _ptr(scores), _ptr(discrete),
                                                        _ptr(kept), _stream(stream)))
 
 
 def compact_pages(p, trig, kept, k_pools, v_pools, block_table, seq_lens, win_start, status, stream=None):
+    nt, L = trig.numel(), len(k_pools)
+    _need("trig", trig, 0, _i32())
+    _step_outputs(p, _units(p, L, nt), None, None, kept)
+    _pools(p, k_pools, "k_pools")
+    _pools(p, v_pools, "v_pools")
+    _tables(p, block_table, seq_lens, win_start)
+    _need("status", status, nt, _i32())
     _check("kara_compact_pages", load().kara_compact_pages(
         ctypes.byref(p), trig.numel(), _ptr(trig), len(k_pools), _ptr(kept), _ptr_array(k_pools),
         _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), _ptr(win_start), _ptr(status), _stream(stream)))
 
 
 def commit_tables(p, trig, block_table, seq_lens, win_start, freed, n_freed, status, stream=None):
+    nt = trig.numel()
+    _need("trig", trig, 0, _i32())
+    _tables(p, block_table, seq_lens, win_start)
+    _need("freed", freed, nt * p.max_blocks_per_seq, _i32())
+    _need("n_freed", n_freed, nt, _i32())
+    _need("status", status, nt, _i32())
     _check("kara_commit_tables", load().kara_commit_tables(
         ctypes.byref(p), trig.numel(), _ptr(trig), _ptr(block_table), _ptr(seq_lens), _ptr(win_start),
         _ptr(freed), _ptr(n_freed), _ptr(status), _stream(stream)))
 
 
+def _compress_checks(p, trig, n_windows, q, k_pools, v_pools, block_table, seq_lens, win_start, status,
+                     scores, discrete, kept, freed, n_freed):
+    nt, L = trig.numel(), len(k_pools)
+    _need("trig", trig, 0, _i32())
+    _need("q", q, L * nt * n_windows * (p.score_queries or p.window) * p.n_q_heads * p.head_dim, _dt(p))
+    _pools(p, k_pools, "k_pools")
+    _pools(p, v_pools, "v_pools")
+    _tables(p, block_table, seq_lens, win_start)
+    _step_outputs(p, _units(p, L, nt, n_windows), scores, discrete, kept)
+    _need("freed", freed, nt * p.max_blocks_per_seq, _i32())
+    _need("n_freed", n_freed, nt, _i32())
+    _need("status", status, nt, _i32())
+
+
 def compress_window(p, trig, q, k_pools, v_pools, block_table, seq_lens, win_start, commit, status,
                     workspace, scores=None, discrete=None, kept=None, freed=None, n_freed=None, stream=None):
+    _compress_checks(p, trig, 1, q, k_pools, v_pools, block_table, seq_lens, win_start, status, scores, discrete,
+                     kept, freed, n_freed)
     _check("kara_compress_window", load().kara_compress_window(
         ctypes.byref(p), trig.numel(), _ptr(trig), len(k_pools), _ptr(q), _ptr_array(k_pools),
         _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), _ptr(win_start), int(bool(commit)),
@@ -270,6 +360,8 @@ def compress_window(p, trig, q, k_pools, v_pools, block_table, seq_lens, win_sta
 def compress_prefill(p, trig, n_windows, q, k_pools, v_pools, block_table, seq_lens, win_start, commit, status,
                      workspace, scores=None, discrete=None, kept=None, freed=None, n_freed=None, stream=None):
     """n_windows consecutive windows of every listed sequence at once (App. C.2)."""
+    _compress_checks(p, trig, int(n_windows), q, k_pools, v_pools, block_table, seq_lens, win_start, status, scores,
+                     discrete, kept, freed, n_freed)
     _check("kara_compress_prefill", load().kara_compress_prefill(
         ctypes.byref(p), trig.numel(), _ptr(trig), int(n_windows), len(k_pools), _ptr(q), _ptr_array(k_pools),
         _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), _ptr(win_start), int(bool(commit)),
@@ -281,6 +373,14 @@ def compress_prefill(p, trig, n_windows, q, k_pools, v_pools, block_table, seq_l
 
 def kv_append(p, seqs, k_new, v_new, k_pools, v_pools, block_table, seq_lens, status, stream=None):
     """Appends k_new / v_new [n_layers][n][n_new][Hkv][d] after each listed sequence's tokens."""
+    n, L = seqs.numel(), len(k_pools)
+    _need("seqs", seqs, 0, _i32())
+    for name, t in (("k_new", k_new), ("v_new", v_new)):
+        _need(name, t, L * n * k_new.shape[2] * p.n_kv_heads * p.head_dim, _dt(p))
+    _pools(p, k_pools, "k_pools")
+    _pools(p, v_pools, "v_pools")
+    _tables(p, block_table, seq_lens)
+    _need("status", status, n, _i32())
     _check("kara_harness_kv_append", load().kara_harness_kv_append(
         ctypes.byref(p), seqs.numel(), _ptr(seqs), k_new.shape[2], len(k_pools), _ptr(k_new), _ptr(v_new),
         _ptr_array(k_pools), _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), _ptr(status),
@@ -297,6 +397,13 @@ def decode_workspace_size(p, n, n_layers, max_len) -> int:
 def decode_attention(p, seqs, q, k_pools, v_pools, block_table, seq_lens, max_len, out, workspace,
                      stream=None):
     """One query per (layer, sequence, query head) over the paged cache; fp32 out of q's shape."""
+    n, L = seqs.numel(), len(k_pools)
+    _need("seqs", seqs, 0, _i32())
+    _need("q", q, L * n * p.n_q_heads * p.head_dim, _dt(p))
+    _need("out", out, L * n * p.n_q_heads * p.head_dim, _f32())
+    _pools(p, k_pools, "k_pools")
+    _pools(p, v_pools, "v_pools")
+    _tables(p, block_table, seq_lens)
     _check("kara_harness_decode_attention", load().kara_harness_decode_attention(
         ctypes.byref(p), seqs.numel(), _ptr(seqs), len(k_pools), _ptr(q), _ptr_array(k_pools),
         _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), max_len, _ptr(out), _ptr(workspace),
@@ -307,6 +414,14 @@ def decode_attention(p, seqs, q, k_pools, v_pools, block_table, seq_lens, max_le
 
 def recompute_attention(p, trig, q, k_pool, v_pool, block_table, seq_lens, win_start, out, status, stream=None):
     """Causal attention of q [n_trig][W][Hq][d] (bf16) over one layer's paged cache into out."""
+    nt = trig.numel()
+    _need("trig", trig, 0, _i32())
+    for name, t in (("q", q), ("out", out)):
+        _need(name, t, nt * p.window * p.n_q_heads * p.head_dim, _dt(p))
+    _pools(p, [k_pool], "k_pool")
+    _pools(p, [v_pool], "v_pool")
+    _tables(p, block_table, seq_lens, win_start)
+    _need("status", status, nt, _i32())
     _check("kara_recompute_attention", load().kara_recompute_attention(
         ctypes.byref(p), trig.numel(), _ptr(trig), _ptr(q), _ptr(k_pool), _ptr(v_pool), _ptr(block_table),
         _ptr(seq_lens), _ptr(win_start), _ptr(out), _ptr(status), _stream(stream)))
@@ -327,7 +442,21 @@ def recompute_queries(p, m: KaraModel, trig, weights, hidden_in, hidden_out, k_p
                       seq_lens, win_start, rope_pos0, q_out, status, workspace, stream=None):
     """The window recompute pass over len(weights) layers; weights: one dict
     per layer of bf16 tensors w_q, w_o, w_gate, w_up, w_down, g_attn, g_ffn."""
-    n = len(weights)
+    n, nt = len(weights), trig.numel()
+    D, F, HD = m.hidden, m.ffn, p.n_q_heads * p.head_dim
+    _need("trig", trig, 0, _i32())
+    for name, t in (("hidden_in", hidden_in), ("hidden_out", hidden_out)):
+        _need(name, t, nt * p.window * D, _f32())
+    _need("q_out", q_out, n * nt * p.window * HD, _dt(p))
+    _need("rope_pos0", rope_pos0, p.n_seqs, _i32())
+    _pools(p, k_pools, "k_pools")
+    _pools(p, v_pools, "v_pools")
+    _tables(p, block_table, seq_lens, win_start)
+    _need("status", status, nt, _i32())
+    sizes = dict(w_q=D * HD, w_o=HD * D, w_gate=D * F, w_up=D * F, w_down=F * D, g_attn=D, g_ffn=D)
+    for i, w in enumerate(weights):
+        for f, size in sizes.items():
+            _need(f"weights[{i}].{f}", w[f], size, _dt(p))
     arr = (LayerWeights * n)()
     for i, w in enumerate(weights):
         arr[i] = LayerWeights(*[_ptr(w[f]).value for f, _ in LayerWeights._fields_])

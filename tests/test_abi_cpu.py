@@ -178,3 +178,26 @@ def test_recompute_host_checks(lib):
                                       None, None, None, None, None, None, 0, None) == kara.ERR_INVALID_ARG
     assert lib.kara_recompute_queries(ctypes.byref(p), ctypes.byref(m), 2, None, 0, w, None, None, None, None, None,
                                       None, None, None, None, None, None, 0, None) == kara.ERR_INVALID_ARG
+
+
+def test_binding_shape_checks():
+    """The binding's host checks (the library cannot see tensor sizes):
+    wrong dtype or too few elements raise before any call."""
+    torch = pytest.importorskip("torch")
+    p = good_params()
+    kara._need("x", None, 10, torch.int32)                     # optional argument left out
+    kara._need("x", torch.zeros(8, dtype=torch.int32), 8, torch.int32)
+    with pytest.raises(kara.KaraError, match="dtype"):
+        kara._need("trig", torch.zeros(8, dtype=torch.int64), 8, torch.int32)
+    with pytest.raises(kara.KaraError, match="at least 9"):
+        kara._need("status", torch.zeros(8, dtype=torch.int32), 9, torch.int32)
+    # the per-step outputs scale with units and the window's compressible length
+    units = kara._units(p, 2, 3)
+    assert units == 2 * 3 * p.n_kv_heads
+    kara._step_outputs(p, units, torch.zeros(units * (p.window - p.buffer)), None, None)
+    with pytest.raises(kara.KaraError, match="kept"):
+        kara._step_outputs(p, units, None, None, torch.zeros(units * p.budget - 1, dtype=torch.int32))
+    with pytest.raises(kara.KaraError, match="block_table"):
+        kara._tables(p, torch.zeros(p.n_seqs * p.max_blocks_per_seq - 1, dtype=torch.int32), None)
+    with pytest.raises(kara.KaraError, match="k_pools"):
+        kara._pools(p, [torch.zeros(4, dtype=torch.bfloat16)], "k_pools")
