@@ -83,6 +83,23 @@ def test_fp32_head128_mha():
     _run(cfg)
 
 
+@pytest.mark.parametrize("head_dim,window", [(64, 1024), (128, 512)])
+def test_fp32_at_its_largest_window(head_dim, window):
+    # fp32 windows hold at most 64K head-dim elements of keys: 1024 keys at
+    # d = 64, 512 at d = 128 (two query heads per KV head)
+    cfg = ki.workload("tiny", n_seqs=2, n_q_heads=4, n_kv_heads=2, head_dim=head_dim, window=window,
+                      budget=window // 5, chunk_budget=8, max_chunk_len=6, num_pages=256, prefix=(3, 90), tail=(0, 9))
+    _run(cfg)
+
+
+def test_more_layers_than_one_launch_takes():
+    # 66 layers: scoring and compaction each run as two launches (64 + 2
+    # layers' pool pointers), the scores and kept rows laid out across both
+    cfg = ki.workload("batch8", n_seqs=2, n_layers=66, n_q_heads=2, n_kv_heads=1, window=128, budget=26,
+                      chunk_budget=4, max_chunk_len=4, prefix=(0, 40), tail=(0, 7), num_pages=64)
+    _run(cfg)
+
+
 @pytest.mark.parametrize("budget,alpha,gamma", [(1024, 16, 8), (205, 0, 8), (300, 64, 3), (1, 0, 3)])
 def test_selection_extremes(budget, alpha, gamma):
     cfg = ki.workload("batch8", n_seqs=2, budget=budget, chunk_budget=alpha, max_chunk_len=gamma)
