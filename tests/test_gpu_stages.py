@@ -57,6 +57,12 @@ def _select_cases():
     a[:, 3::7] = 0.0
     yield "signed", a
     yield "equal", np.full((2, 300), 0.5, dtype=np.float32)
+    # past 2048 positions the 16-position instance runs: ties and equal
+    # scores there too, at a ragged length and at the largest one
+    yield "ties_2049", rng.integers(0, 4, (3, 2049)).astype(np.float32)
+    yield "ties_4096", rng.integers(0, 4, (3, 4096)).astype(np.float32)
+    yield "equal_4096", np.full((2, 4096), 0.25, dtype=np.float32)
+    yield "random_4096", rng.random((3, 4096)).astype(np.float32)
 
 
 @pytest.mark.parametrize("name,scores", list(_select_cases()), ids=lambda x: x if isinstance(x, str) else "")
