@@ -54,16 +54,16 @@ struct ACfg {
   static constexpr int kCPR = kRowBytes / 16;          // 16-byte chunks per row
   static constexpr int kSwz = kCPR - 1;
   // XOR swizzles of a row's 16-byte chunks.  K (read 16 rows x 16 bytes per
-  // lane group): by the row, its two 2-bit halves swapped at d = 128.  V
+  // lane group): by the row with its two low bits moved to the top.  V
   // (read through the transposed load, 32 lanes x 8 bytes at a time over 8
   // rows and two adjacent chunks): by twice the row (twice its half at
   // d = 64, whose rows are half a bank sweep), so the 16 (row, chunk) pairs
-  // of such a read land in 16 distinct chunks.  Both measured on gfx950
-  // (d = 128) free of bank conflicts; XOR by the row itself costs about four
-  // conflict cycles per K read and two per V read.
+  // of such a read land in 16 distinct chunks.  Measured on gfx950 free of
+  // bank conflicts (K at d = 64 and 128, V at d = 128); XOR by the row itself
+  // costs about four conflict cycles per K read and two per V read.
   static __device__ __forceinline__ int swz_k(int row) {
     if constexpr (D == 128) return ((row & 3) << 2) | ((row >> 2) & 3);
-    return row & kSwz;
+    return ((row & 3) << 1) | ((row >> 2) & 1);
   }
   static __device__ __forceinline__ int swz_v(int row) { return (2 * (D == 128 ? row : row >> 1)) & kSwz; }
   static constexpr int kKS = kCPR / 4;                 // k-steps of one dot product (per lane group)

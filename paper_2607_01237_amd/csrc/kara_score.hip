@@ -72,13 +72,14 @@ struct Cfg {
   static constexpr int kRowBytes = D * kES;              // one key or query row
   static constexpr int kCPR = kRowBytes / 16;            // 16-byte chunks per row
   static constexpr int kSwz = kCPR < 16 ? kCPR - 1 : 15; // XOR swizzle mask
-  // XOR swizzle of a key row's 16-byte chunks, a function of the row.  For
-  // 256-byte rows (bf16, d = 128) the row's two 2-bit halves are swapped
-  // first: measured on gfx950, a 16-byte read of 16 rows x 4 lane groups then
-  // has no bank conflicts, where XOR by the row itself costs about four
-  // conflict cycles per read.
+  // XOR swizzle of a key row's 16-byte chunks, a function of the row, with
+  // the row's two low bits moved to the top: measured on gfx950, a 16-byte
+  // read of 16 rows x 4 lane groups then has no bank conflicts, where XOR by
+  // the row itself costs about four conflict cycles per read (256-byte rows:
+  // bf16 d = 128, fp32 d = 64; 128-byte rows: bf16 d = 64).
   static __device__ __forceinline__ int swz(int row) {
     if constexpr (kCPR == 16) return ((row & 3) << 2) | ((row >> 2) & 3);
+    if constexpr (kCPR == 8) return ((row & 3) << 1) | ((row >> 2) & 1);
     return row & kSwz;
   }
   static constexpr int kRowsWG = kScoreWaves * 16 * RT;  // query rows per workgroup
