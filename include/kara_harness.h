@@ -62,9 +62,10 @@ kara_status_t kara_harness_decode_workspace_size(const kara_params_t* p, int32_t
  * G = n_q_heads / n_kv_heads <= KARA_HARNESS_MAX_GROUP; scale = p->scale, or
  * 1/sqrt(head_dim)).  q: [n_layers][n][n_q_heads][head_dim] (p->dtype); out:
  * fp32, same shape.  Sequences must be at most max_len tokens long (the
- * value the workspace was sized for); longer ones, and empty ones, give zero
- * output rows.  Pages are not checked: the block table must map every
- * position below seq_len to a page of the pool.
+ * value the workspace was sized for); longer ones, empty ones and sequence
+ * indices outside [0, n_seqs) give zero output rows.  Pages are not checked:
+ * the block table must map every position below seq_len to a page of the
+ * pool.
  */
 kara_status_t kara_harness_decode_attention(const kara_params_t* p, int32_t n, const int32_t* seqs,
                                             int32_t n_layers, const void* q,

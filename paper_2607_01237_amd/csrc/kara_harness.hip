@@ -144,6 +144,7 @@ __global__ __launch_bounds__(64) void decode_split_kernel(Geom g, int n, const i
   const int j = (int)((rest / g.Hkv) % n);
   const int l = (int)(rest / ((int64_t)g.Hkv * n));
   const int s = seqs[j];
+  if (s < 0 || s >= g.n_seqs) return;   // the combine kernel writes its zero rows
   const int len = seq_lens[s];
   const int k0 = split * kSplitKeys;
   if (len <= 0 || len > max_len || k0 >= len) return;
@@ -265,7 +266,8 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(Geom g, int n, const
   const int lane = threadIdx.x;
   const int64_t row = blockIdx.x;                 // (l, j, hq)
   const int j = (int)((row / g.Hq) % n);
-  const int len = seq_lens[seqs[j]];
+  const int s = seqs[j];
+  const int len = s >= 0 && s < g.n_seqs ? seq_lens[s] : 0;
   float* dst = out + row * D + lane * kDPerLane;
   if (len <= 0 || len > max_len) {
 #pragma unroll

@@ -59,7 +59,8 @@ def test_decode_attention(dtype, Hq, Hkv, d):
     g = torch.Generator(device="cpu").manual_seed(5)
     kp = [torch.randn((p["num_pages"], Hkv, bs, d), generator=g).to(dt) for _ in range(L)]
     vp = [torch.randn((p["num_pages"], Hkv, bs, d), generator=g).to(dt) for _ in range(L)]
-    seqs = np.array([5, 0, 3, 1, 4, 2, 6, 7], dtype=np.int32)[:7]      # seq 7 is not listed
+    # seq 7 is not listed; len(lens) and -1 are indices outside the table (zero rows)
+    seqs = np.array([5, 0, 3, 1, 4, 2, 6, len(lens), -1], dtype=np.int32)
     n = len(seqs)
     q = torch.randn((L, n, Hq, d), generator=g).to(dt)
     T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
@@ -77,6 +78,9 @@ def test_decode_attention(dtype, Hq, Hkv, d):
     for l in range(L):
         kh, vh = _f64(ki.raw_numpy(kp[l]), dtype), _f64(ki.raw_numpy(vp[l]), dtype)
         for j, s in enumerate(seqs):
+            if s < 0 or s >= len(lens):
+                assert (got[l, j] == 0).all(), f"sequence index {s} is outside the table: zero rows"
+                continue
             n_tok = int(lens[s])
             if n_tok == 0 or n_tok > max_len:
                 assert (got[l, j] == 0).all(), f"seq {s} should give zero rows"
