@@ -274,7 +274,7 @@ def dest_rows(geom, p, n_windows):
     return np.concatenate(pages), np.concatenate(slots)
 
 
-def cpu_baseline(geom, p, q, kp, vp, budget_s, n_windows=1):
+def cpu_baseline(geom, p, q, kp, vp, budget_s, n_windows=1, threads=None):
     """The oracle, as it stands, on whole units of the workload.
 
     Units of layer 0 (sequence by sequence, window by window, every KV head)
@@ -287,7 +287,8 @@ def cpu_baseline(geom, p, q, kp, vp, budget_s, n_windows=1):
 
     import oracle
 
-    threads = min(16, len(os.sched_getaffinity(0)))
+    if threads is None:
+        threads = min(16, len(os.sched_getaffinity(0)))
     W, U = p["window"], p["buffer"]
     N = W - U
     scale = oracle.scale_of(p)
@@ -303,7 +304,9 @@ def cpu_baseline(geom, p, q, kp, vp, budget_s, n_windows=1):
     H = p["n_kv_heads"]
     all_units = [(0, t, w, h) for t in range(len(geom.trig)) for w in range(n_windows) for h in range(H)]
     done, busy = 0, 0.0
-    with ThreadPoolExecutor(threads) as ex:
+    # one BLAS thread per worker, so that `threads` is the number of cores used
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(limits=1), ThreadPoolExecutor(threads) as ex:
         for i in range(0, len(all_units), threads):
             batch = all_units[i:i + threads]
             hq, hk, hv = host_units(geom, p, q, kp, vp, batch, n_windows)
@@ -918,11 +921,15 @@ def main():
         done, dt_cpu, threads = cpu_baseline(geom, p, q, kp, vp, args.cpu_seconds, nw)
         # units per window token: every window token is compressed in L*H units
         rate = done / dt_cpu * W / (L * H)
+        # the same oracle on one thread, over a quarter of the time
+        done1, dt1, _ = cpu_baseline(geom, p, q, kp, vp, args.cpu_seconds / 4, nw, threads=1)
         result["cpu_baseline"] = {
             "value": rate, "unit": "window tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"{done} whole (sequence, window, KV head) units of layer 0 of this workload: fp64 scoring, "
                       f"selection, Token2Chunk, fill and K/V gather in {dt_cpu:.1f} s of oracle time; one window "
                       f"token is compressed in layers*kv_heads units, so rate = units/s * W/(layers*kv_heads)",
+            "value_one_core": done1 / dt1 * W / (L * H),
+            "sample_one_core": f"{done1} units on one thread in {dt1:.1f} s",
         }
     print(json.dumps(result), flush=True)
 
