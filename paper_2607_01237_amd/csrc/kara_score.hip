@@ -444,12 +444,19 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(ScoreArgs a) {
       v[ti] = sum;
     }
     // over the four lane groups, leaving lane group gq with tile gq:
-    // groups {0,1} keep tiles 0,1 and {2,3} keep tiles 2,3, then pairs split
-    const bool lo_half = gq < 2;
-    const float x0 = (lo_half ? v[0] : v[2]) + __shfl_xor(lo_half ? v[2] : v[0], 32, 64);
-    const float x1 = (lo_half ? v[1] : v[3]) + __shfl_xor(lo_half ? v[3] : v[1], 32, 64);
-    const bool odd = gq & 1;
-    const float y = (odd ? x1 : x0) + __shfl_xor(odd ? x0 : x1, 16, 64);
+    // groups {0,1} keep tiles 0,1 and {2,3} keep tiles 2,3, then pairs split.
+    // The exchanges are register swaps between lane halves and between
+    // 16-lane rows: after permlane32_swap(a, b), the first result holds a's
+    // low half and b's low half, the second a's high half and b's high
+    // half, so their sum is tile a's pair sum in lanes 0-31 and tile b's in
+    // lanes 32-63; permlane16_swap does the same for even and odd rows.
+    static_assert(kTps == 4, "the reduce-scatter covers four key tiles");
+    const auto s0 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[0]), __float_as_uint(v[2]), false, false);
+    const auto s1 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v[1]), __float_as_uint(v[3]), false, false);
+    const float x0 = __uint_as_float(s0[0]) + __uint_as_float(s0[1]);
+    const float x1 = __uint_as_float(s1[0]) + __uint_as_float(s1[1]);
+    const auto s2 = __builtin_amdgcn_permlane16_swap(__float_as_uint(x0), __float_as_uint(x1), false, false);
+    const float y = __uint_as_float(s2[0]) + __uint_as_float(s2[1]);
     col_wave[ch % kColSlots][wave][gq * 16 + li] = y;
   };
   // the eight waves' sums of one chunk, added in wave order
