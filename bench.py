@@ -4,12 +4,11 @@ A step is the whole path -- validation, window scoring, discrete TopK,
 Token2Chunk + fill, in-place compaction of K and V, metadata commit -- for
 every triggered sequence, layer and KV head of one batch, through
 kara_compress_window.  Inputs are resident in HBM before timing starts.
-Between steps only the block table and sequence lengths are restored (a few
-hundred KB, device to device, inside the timed loop); the window's K/V rows
-keep whatever the previous step left, so every step compresses a full
-window of the same shape.  The staged pass restores those rows too, from a
-device backup and outside its events, so each of its passes compresses the
-same input.
+Before every step (warm-up, timed and staged alike) the block table, the
+sequence lengths and every K/V row compaction can overwrite are restored
+from a device backup, outside the timed region, so every step compresses
+the same fresh input; HIP events on the launch stream bracket the
+compression call alone.
 
 Prints one JSON line.  `value` is window tokens compressed per second
 (triggered sequences x windows x window length per step / step time).  `roofline`
@@ -277,8 +276,8 @@ def dest_rows(geom, p, n_windows):
 def cpu_baseline(geom, p, q, kp, vp, budget_s, n_windows=1, threads=None):
     """The oracle, as it stands, on whole units of the workload.
 
-    Units of layer 0 (sequence by sequence, window by window, every KV head)
-    are copied to the host in batches and run through the oracle's scoring,
+    Units in layer order (sequence by sequence, window by window, every KV
+    head, then the next layer) are copied to the host in batches and run through the oracle's scoring,
     selection, Token2Chunk, fill and K/V gather until `budget_s` seconds have
     passed.  With one window a unit's rows are its window and the tail after
     it; with several, the unit's own window.
@@ -288,6 +287,8 @@ def cpu_baseline(geom, p, q, kp, vp, budget_s, n_windows=1, threads=None):
     import oracle
 
     if threads is None:
+        # one GPU's share of the host: the GPU machines allot 16 cores per GPU,
+        # whatever the affinity mask shows
         threads = min(16, len(os.sched_getaffinity(0)))
     W, U = p["window"], p["buffer"]
     N = W - U
@@ -302,7 +303,9 @@ def cpu_baseline(geom, p, q, kp, vp, budget_s, n_windows=1, threads=None):
         return 1
 
     H = p["n_kv_heads"]
-    all_units = [(0, t, w, h) for t in range(len(geom.trig)) for w in range(n_windows) for h in range(H)]
+    # layer by layer until the time budget is spent
+    all_units = [(l, t, w, h) for l in range(len(kp)) for t in range(len(geom.trig)) for w in range(n_windows)
+                 for h in range(H)]
     done, busy = 0, 0.0
     # one BLAS thread per worker, so that `threads` is the number of cores used
     from threadpoolctl import threadpool_limits
@@ -745,11 +748,8 @@ def main():
         meta["seq_lens"].copy_(meta["seq_lens0"], non_blocking=True)
 
     # Device backup of the rows compaction overwrites, taken before any step:
-    # each staged pass below starts from the same pools (restored outside
-    # its events), so every pass compresses the same input.  The timed steps
-    # run back to back on the pools the previous step left; scoring and
-    # selection cost does not depend on that, and compaction skips the kept
-    # rows that are already in place.
+    # every step below starts from the same pools and tables (restored
+    # outside its events), so every step compresses the same input.
     pg, sl = (torch.from_numpy(a).to(device) for a in dest_rows(geom, p, nw))
     backup = [(k[pg, :, sl, :], v[pg, :, sl, :]) for k, v in zip(kp, vp)]
     log(f"pool backup: {len(pg)} rows per layer, {sum(b.numel() * b.element_size() for kv in backup for b in kv) / 1e9:.2f} GB")
@@ -768,9 +768,6 @@ def main():
                                   meta["win_start"], True, status, ws, kept=kept, freed=freed, n_freed=n_freed,
                                   stream=stream)
 
-    def step():
-        restore()
-        compress()
 
     # The staged pass times scoring and selection through the single-window
     # entry points.  Prefill's windows are scored as separate sequences then:
@@ -801,25 +798,42 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    es = 2 if p["dtype"] == "bf16" else 4
+    row_bytes = p["head_dim"] * es
+    tails = (geom.seq_lens[geom.trig] - geom.win_start[geom.trig] - (nw - 1) * N - W).astype(np.int64)
+
+    def moved_gb():
+        """Compaction's algorithmic bytes of the step just run, each way."""
+        rows = moved_rows(kept.cpu().numpy().reshape(L, nt, nw, H, p["budget"]), p, tails).sum()
+        return float(rows) * row_bytes * 2 / 1e9
+
     for _ in range(args.warmup):
-        step()
+        restore()
+        restore_pools()
+        compress()
     torch.cuda.synchronize()
     log("warmup done")
 
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    step_gb = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
+        restore()
+        restore_pools()
         ev[i][0].record(stream)
-        step()
+        compress()
         ev[i][1].record(stream)
-    torch.cuda.synchronize()
+        torch.cuda.synchronize()
+        step_gb.append(moved_gb())
     wall = time.perf_counter() - t0
     step_ms = [a.elapsed_time(b) for a, b in ev]
     st = status.cpu().numpy()
     assert (st == 0).all(), f"unexpected status {st}"
-    log(f"timed {args.steps} steps: wall {wall * 1e3 / args.steps:.3f} ms/step, events median "
-        f"{np.median(step_ms):.3f} ms")
+    assert len(set(round(x, 6) for x in step_gb)) == 1, f"steps moved different bytes: {step_gb}"
+    log(f"timed {args.steps} steps: events mean {np.mean(step_ms):.3f} ms, median {np.median(step_ms):.3f} ms; "
+        f"compaction moved {step_gb[0]:.4f} GB each way in every step; wall incl. restores "
+        f"{wall * 1e3 / args.steps:.3f} ms/step")
 
     # staged pass: the same path through the per-stage entry points, with HIP
     # events between stages on the launch stream.  With several windows the
@@ -829,7 +843,6 @@ def main():
     stages = ["score", "select_t2c", "compact", "commit"]
     times = {s: [] for s in stages}
     moved = []
-    tails = (geom.seq_lens[geom.trig] - geom.win_start[geom.trig] - (nw - 1) * N - W).astype(np.int64)
     n_stage = max(3, args.steps)
     for i in range(n_stage + 1):
         restore()
@@ -871,8 +884,6 @@ def main():
     flops = 2.0 * units * nw * G * Wq * N * p["head_dim"]
     peak = PEAK_BF16_TFLOPS if p["dtype"] == "bf16" else PEAK_F32_TFLOPS
     ach = flops / (avg["score"] * 1e-3) / 1e12
-    es = 2 if p["dtype"] == "bf16" else 4
-    row_bytes = p["head_dim"] * es
     # read + write, K and V, averaged over the passes timed
     compact_bytes = float(np.mean(moved)) * row_bytes * 2 * 2
     log("compaction algorithmic GB per staged pass (read = write): "
@@ -881,7 +892,7 @@ def main():
     sc_ms = avg["select_t2c"] + avg["compact"]
     sc_gbs = (compact_bytes + select_bytes) / (sc_ms * 1e-3) / 1e9
 
-    ms = wall * 1e3 / args.steps
+    ms = float(np.mean(step_ms))
     win_tokens = nt * nw * W
     traffic = load_traffic(args.workload)
     result = {
@@ -893,6 +904,8 @@ def main():
         "warmup": args.warmup,
         "ms_per_step": ms,
         "ms_per_step_events_median": float(np.median(step_ms)),
+        "ms_per_step_wall_incl_restores": wall * 1e3 / args.steps,
+        "compaction_gb_each_way_per_step": step_gb,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -925,7 +938,9 @@ def main():
         done1, dt1, _ = cpu_baseline(geom, p, q, kp, vp, args.cpu_seconds / 4, nw, threads=1)
         result["cpu_baseline"] = {
             "value": rate, "unit": "window tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"{done} whole (sequence, window, KV head) units of layer 0 of this workload: fp64 scoring, "
+            "host_cpus_visible": len(os.sched_getaffinity(0)), "host_cpu_count": os.cpu_count(),
+            "cores_note": "16 worker threads, one BLAS thread each: the host share one GPU is allotted",
+            "sample": f"{done} whole (layer, sequence, window, KV head) units of this workload, in layer order: fp64 scoring, "
                       f"selection, Token2Chunk, fill and K/V gather in {dt_cpu:.1f} s of oracle time; one window "
                       f"token is compressed in layers*kv_heads units, so rate = units/s * W/(layers*kv_heads)",
             "value_one_core": done1 / dt1 * W / (L * H),

@@ -25,10 +25,21 @@
  *     work; none synchronises.
  *   - Return codes report host-checkable argument errors only; on error
  *     nothing is enqueued.  Data-dependent problems of a triggered sequence
- *     (window outside the sequence, page id outside the pool, the sequence
- *     triggered twice, sequence index out of range) are written to the
- *     device array `status[t]` (KARA_SEQ_* bits); such a sequence gets zero
- *     scores and is neither compacted nor committed.
+ *     (window outside the sequence, page id outside the pool, a page mapped
+ *     twice, the sequence triggered twice, sequence index out of range) are
+ *     written to the device array `status[t]` (KARA_SEQ_* bits); such a
+ *     sequence gets zero scores and is neither compacted nor committed.
+ *   - Page ownership: compaction moves rows in place, so the pages holding a
+ *     triggered sequence's window and tail must belong to that sequence
+ *     alone.  A page mapped twice inside one sequence is flagged
+ *     (KARA_SEQ_DUP_PAGE); a page shared between two sequences is not
+ *     checked and must not occur (no prefix sharing of window pages).
+ *   - status lifetime within one event: kara_validate, kara_score_window,
+ *     kara_compress_window and kara_compress_prefill rewrite status[t]
+ *     from scratch.  kara_compact_pages and kara_commit_tables keep a
+ *     KARA_SEQ_BAD_KEPT bit already set, so a bad kept set found in any
+ *     layer's compaction call stops the commit of that sequence; start an
+ *     event with one of the former calls.
  *   - kara_token2chunk writes -1 to every kept entry of a unit whose discrete
  *     row is not strictly ascending inside [0, window - buffer).
  *   - Ordering: every ranking is by (value descending, index ascending).
@@ -91,6 +102,9 @@ typedef enum kara_status {
 #define KARA_SEQ_DUP_TRIGGER 4  /* the sequence appears more than once in trig */
 #define KARA_SEQ_BAD_INDEX 8    /* trig[t] outside [0, n_seqs) */
 #define KARA_SEQ_BAD_KEPT 16    /* kara_compact_pages: a kept row not ascending or outside [0, window-buffer) */
+#define KARA_SEQ_DUP_PAGE 32    /* a page of the blocks compaction writes ([win_start/block_size,
+                                   ceil(seq_len/block_size))) appears twice among the sequence's
+                                   blocks [0, ceil(seq_len/block_size)) */
 
 /*
  * Window and cache geometry (Kara Sec. 4.1, Eq. (5) and (7); App. C.4).
@@ -140,6 +154,14 @@ const char* kara_status_string(int32_t status);
 
 /* KARA_ABI_VERSION of the loaded library. */
 int32_t kara_abi_version(void);
+
+/*
+ * Build provenance (not part of the method): hex SHA-256 over the sources,
+ * headers and compile options this library was built from, or "unknown".
+ * A caller holding the sources can recompute it to make sure the loaded
+ * binary is current.  Static storage; never freed by the caller.
+ */
+const char* kara_source_hash(void);
 
 /*
  * Text of the HIP error behind the most recent KARA_ERR_HIP returned on the
@@ -196,9 +218,15 @@ kara_status_t kara_token2chunk(const kara_params_t* p, int64_t n_units, const fl
  * Window gather, Eq. (9), in place in the paged pools of n_layers layers:
  * window-relative row j receives row kept[j] for j < budget, then the buffer
  * rows, then the tail rows (each K and V head independently).  Writes status
- * (validation runs first).  Does not touch block_table or seq_lens: call
- * kara_commit_tables once after every layer has been compacted.  Compacting
- * the same layer twice before committing is a caller error.
+ * (validation runs first; a KARA_SEQ_BAD_KEPT bit already in status[t] is
+ * kept, and a sequence with any bit set is not compacted).  Does not touch
+ * block_table or seq_lens: call kara_commit_tables once after every layer
+ * has been compacted.  Compacting the same layer twice before committing is
+ * a caller error.  When layers are compacted one call at a time and a later
+ * call finds a bad kept set, the layers compacted by earlier calls stay
+ * compacted and the commit skips the sequence: its cache is then
+ * inconsistent and must be rebuilt by the caller (the check of all layers'
+ * kept sets before any compaction is one call over all layers).
  */
 kara_status_t kara_compact_pages(const kara_params_t* p, int32_t n_trig, const int32_t* trig,
                                  int32_t n_layers, const int32_t* kept, void* const* k_pools,
@@ -210,7 +238,8 @@ kara_status_t kara_compact_pages(const kara_params_t* p, int32_t n_trig, const i
  * Metadata update of Algorithm 1: new seq_len = seq_len - (window - buffer -
  * budget); the logical blocks no longer covered are released (page ids into
  * freed[t][*] in ascending block order, table entries set to -1).  Writes
- * status (validation runs first); flagged sequences are left unchanged.
+ * status (validation runs first, keeping a KARA_SEQ_BAD_KEPT bit set by this
+ * event's kara_compact_pages calls); flagged sequences are left unchanged.
  */
 kara_status_t kara_commit_tables(const kara_params_t* p, int32_t n_trig, const int32_t* trig,
                                  int32_t* block_table, int32_t* seq_lens,

@@ -55,6 +55,7 @@ SEQ_BAD_WINDOW = 1
 SEQ_BAD_PAGE = 2
 SEQ_DUP_TRIGGER = 4
 SEQ_BAD_INDEX = 8
+SEQ_DUP_PAGE = 32
 
 
 # ---------------------------------------------------------------- elements
@@ -244,6 +245,13 @@ def validate(p: dict, trig: np.ndarray, block_table: np.ndarray, seq_lens: np.nd
         pages = block_table[s, p0 // bs: -(-L // bs)]
         if np.any(pages < 0) or np.any(pages >= p["num_pages"]):
             status[t] |= SEQ_BAD_PAGE
+        # R-PAGES: compaction rewrites the window's pages in place, so each
+        # page it writes must hold no other block of the sequence
+        row = block_table[s, :-(-L // bs)]
+        for b in range(p0 // bs, len(row)):
+            if 0 <= row[b] < p["num_pages"] and np.any(row[:b] == row[b]):
+                status[t] |= SEQ_DUP_PAGE
+                break
     return status
 
 

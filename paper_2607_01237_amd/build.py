@@ -39,6 +39,28 @@ FLAGS = [
 FILE_FLAGS = {
     "kara_select.hip": ["-mllvm", "-amdgpu-promote-alloca-to-vector-limit=256"],
 }
+# rocBLAS runs the recompute pass's plain matrix products
+LINK_LIBS = ["-L/opt/rocm/lib", "-lrocblas"]
+
+
+def source_hash() -> str:
+    """SHA-256 over every source, header and compile option the library is
+    built from.  The build bakes it into libkara.so (kara_source_hash) and the
+    binding compares it at load time, so a library built from other sources
+    is refused instead of silently tested."""
+    import hashlib
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(CSRC, "*")) + glob.glob(os.path.join(INCLUDE, "*.h")))
+    for path in files:
+        if os.path.isfile(path):
+            h.update(os.path.basename(path).encode())
+            with open(path, "rb") as f:
+                h.update(f.read())
+    # options with the checkout's location taken out, so the same tree hashes
+    # the same wherever it sits
+    flags = [f.replace(ROOT, "<root>") for f in FLAGS]
+    h.update(repr((ARCH, flags, sorted(FILE_FLAGS.items()), LINK_LIBS)).encode())
+    return h.hexdigest()
 
 
 def _run(cmd):
@@ -54,16 +76,17 @@ def build(verbose: bool = False) -> str:
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
     objs = [os.path.join(BUILD, os.path.basename(s) + ".o") for s in srcs]
 
+    digest = source_hash()
+
     def compile_one(pair):
         src, obj = pair
-        return _run([HIPCC, *FLAGS, *FILE_FLAGS.get(os.path.basename(src), []), "-c", src, "-o", obj])
+        extra = [f'-DKARA_SOURCE_HASH="{digest}"'] if os.path.basename(src) == "kara_api.cpp" else []
+        return _run([HIPCC, *FLAGS, *FILE_FLAGS.get(os.path.basename(src), []), *extra, "-c", src, "-o", obj])
 
     with ThreadPoolExecutor(min(8, len(srcs))) as ex:
         outs = list(ex.map(compile_one, zip(srcs, objs)))
     tmp = LIB + ".tmp"
-    # rocBLAS runs the recompute pass's plain matrix products
-    outs.append(_run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-L/opt/rocm/lib", "-lrocblas",
-                      "-o", tmp]))
+    outs.append(_run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, *LINK_LIBS, "-o", tmp]))
     os.replace(tmp, LIB)
     if verbose:
         for o in outs:

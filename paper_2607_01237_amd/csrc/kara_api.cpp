@@ -179,7 +179,7 @@ kara_status_t compress(const kara_params_t* p, int32_t n_trig, const int32_t* tr
   int32_t* kept_buf = kept ? kept : (int32_t*)(ws + wl.kept);
   hipStream_t s = (hipStream_t)stream;
 
-  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, s);
+  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, false, s);
   if (e == hipSuccess)
     e = run_score(g, sp, n_layers, q, (const void* const*)k_pools, trig, block_table, win_start, status,
                   partials, scores_buf, s);
@@ -212,6 +212,11 @@ const char* kara_status_string(int32_t s) {
 
 int32_t kara_abi_version(void) { return KARA_ABI_VERSION; }
 
+#ifndef KARA_SOURCE_HASH
+#define KARA_SOURCE_HASH "unknown"
+#endif
+const char* kara_source_hash(void) { return KARA_SOURCE_HASH; }
+
 const char* kara_last_hip_error(void) {
   return t_last_hip_error == hipSuccess ? "no HIP error" : hipGetErrorString(t_last_hip_error);
 }
@@ -236,7 +241,7 @@ kara_status_t kara_validate(const kara_params_t* p, int32_t n_trig, const int32_
   if (n_trig == 0) return KARA_OK;
   if (!trig || !block_table || !seq_lens || !win_start || !status) return KARA_ERR_INVALID_ARG;
   return hip_status(
-      launch_validate(g, trig, block_table, seq_lens, win_start, status, (hipStream_t)stream));
+      launch_validate(g, trig, block_table, seq_lens, win_start, status, false, (hipStream_t)stream));
 }
 
 kara_status_t kara_score_window(const kara_params_t* p, int32_t n_trig, const int32_t* trig,
@@ -258,7 +263,7 @@ kara_status_t kara_score_window(const kara_params_t* p, int32_t n_trig, const in
   if (!workspace || workspace_bytes < wl.total) return KARA_ERR_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
   char* ws = (char*)workspace;
-  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, s);
+  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, false, s);
   if (e == hipSuccess)
     e = run_score(g, sp, n_layers, q, k_pools, trig, block_table, win_start, status, (float*)(ws + wl.partials),
                   scores, s);
@@ -303,7 +308,7 @@ kara_status_t kara_compact_pages(const kara_params_t* p, int32_t n_trig, const i
       !pools_ok((const void* const*)k_pools, n_layers) || !pools_ok((const void* const*)v_pools, n_layers))
     return KARA_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, s);
+  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, true, s);
   if (e == hipSuccess) e = launch_check_kept(g, n_layers, kept, status, s);
   if (e == hipSuccess)
     e = run_compact(g, n_layers, trig, kept, k_pools, v_pools, block_table, seq_lens, win_start, status, s);
@@ -321,7 +326,7 @@ kara_status_t kara_commit_tables(const kara_params_t* p, int32_t n_trig, const i
   if (!trig || !block_table || !seq_lens || !win_start || !freed || !n_freed || !status)
     return KARA_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)stream;
-  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, s);
+  hipError_t e = launch_validate(g, trig, block_table, seq_lens, win_start, status, true, s);
   if (e == hipSuccess) e = launch_commit(g, trig, block_table, seq_lens, win_start, freed, n_freed, status, s);
   return hip_status(e);
 }

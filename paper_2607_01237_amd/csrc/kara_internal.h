@@ -40,10 +40,11 @@ kara_status_t make_geom(const kara_params_t* p, int32_t n_trig, Geom* g);
 kara_status_t hip_status(hipError_t e);
 bool pools_ok(const void* const* pools, int n_layers);
 
-// Validation kernel (kara_pages.hip).
+// Validation kernel (kara_pages.hip).  keep_kept: a KARA_SEQ_BAD_KEPT bit
+// already in status survives (staged per-layer compaction and the commit).
 hipError_t launch_validate(const Geom& g, const int32_t* trig, const int32_t* block_table,
                            const int32_t* seq_lens, const int32_t* win_start, int32_t* status,
-                           hipStream_t stream);
+                           bool keep_kept, hipStream_t stream);
 
 // Scoring (kara_score.hip): per unit, n_splits workgroups each write a
 // partial column sum into `partials`, and a second kernel adds them in split

@@ -6,41 +6,66 @@
 namespace kara {
 namespace {
 
-__global__ void validate_kernel(Geom g, const int32_t* __restrict__ trig,
-                                const int32_t* __restrict__ bt, const int32_t* __restrict__ seq_lens,
-                                const int32_t* __restrict__ win_start, int32_t* __restrict__ status) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= g.n_trig) return;
-  const int t = (int)i;
+// One workgroup per listed sequence.  Besides the window and page-range
+// checks, no page of the blocks compaction writes ([p0/bs, ceil(len/bs)))
+// may appear twice among the sequence's blocks [0, ceil(len/bs)): compaction
+// moves rows in place, and a page mapped twice would be read and written by
+// two workgroups at once.  keep_kept: a KARA_SEQ_BAD_KEPT bit already in
+// status[t] survives (the staged per-layer calls of one event).
+constexpr int kValidateThreads = 256;
+constexpr int kValidateRowLds = 8192;   // table entries staged in LDS (32 KB)
+
+__global__ __launch_bounds__(kValidateThreads) void validate_kernel(
+    Geom g, const int32_t* __restrict__ trig, const int32_t* __restrict__ bt,
+    const int32_t* __restrict__ seq_lens, const int32_t* __restrict__ win_start,
+    int32_t* __restrict__ status, int keep_kept) {
+  const int t = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int kept_bit = keep_kept ? (status[t] & KARA_SEQ_BAD_KEPT) : 0;
+  // every thread has read status[t] before thread 0 rewrites it
+  __syncthreads();
   const int s = trig[t];
   if (s < 0 || s >= g.n_seqs) {
-    status[t] = KARA_SEQ_BAD_INDEX;
+    if (tid == 0) status[t] = KARA_SEQ_BAD_INDEX | kept_bit;
     return;
   }
-  int st = 0;
-  for (int o = 0; o < g.n_trig; ++o)
-    if (o != t && trig[o] == s) {
-      st |= KARA_SEQ_DUP_TRIGGER;
-      break;
-    }
+  int dup = 0;
+  for (int o = tid; o < g.n_trig; o += kValidateThreads)
+    if (o != t && trig[o] == s) dup = 1;
+  const int st0 = (__syncthreads_or(dup) ? KARA_SEQ_DUP_TRIGGER : 0) | kept_bit;
   const int p0 = win_start[s];
   const int len = seq_lens[s];
   // the windows cover [p0, p0 + (n_win-1)*N + W)
   if (p0 < 0 || (int64_t)p0 + (int64_t)(g.n_win - 1) * g.N + g.W > (int64_t)len ||
       (int64_t)len > (int64_t)g.max_blocks * g.bs) {
-    status[t] = st | KARA_SEQ_BAD_WINDOW;
+    if (tid == 0) status[t] = st0 | KARA_SEQ_BAD_WINDOW;
     return;
   }
   const int32_t* row = bt + (int64_t)s * g.max_blocks;
+  const int b0 = p0 / g.bs;
   const int b1 = (len + g.bs - 1) / g.bs;
-  for (int b = p0 / g.bs; b < b1; ++b) {
-    const int pg = row[b];
+  // the table row in LDS when it fits (the pairwise scan reads it often)
+  __shared__ int32_t row_lds[kValidateRowLds];
+  const bool in_lds = b1 <= kValidateRowLds;
+  if (in_lds)
+    for (int b = tid; b < b1; b += kValidateThreads) row_lds[b] = row[b];
+  __syncthreads();
+  int bad = 0, twice = 0;
+  for (int b = b0 + tid; b < b1; b += kValidateThreads) {
+    const int pg = in_lds ? row_lds[b] : row[b];
     if (pg < 0 || pg >= g.num_pages) {
-      st |= KARA_SEQ_BAD_PAGE;
-      break;
+      bad = 1;
+      continue;
+    }
+    if (in_lds) {
+      for (int c = 0; c < b; ++c) twice |= row_lds[c] == pg;
+    } else {
+      for (int c = 0; c < b; ++c) twice |= row[c] == pg;
     }
   }
-  status[t] = st;
+  const int st = st0 | (__syncthreads_or(bad) ? KARA_SEQ_BAD_PAGE : 0) |
+                 (__syncthreads_or(twice) ? KARA_SEQ_DUP_PAGE : 0);
+  if (tid == 0) status[t] = st;
 }
 
 // Flags triggered sequences whose kept rows (caller-supplied) are not a
@@ -171,11 +196,10 @@ __global__ void commit_kernel(Geom g, const int32_t* __restrict__ trig, int32_t*
 
 hipError_t launch_validate(const Geom& g, const int32_t* trig, const int32_t* block_table,
                            const int32_t* seq_lens, const int32_t* win_start, int32_t* status,
-                           hipStream_t stream) {
-  const int threads = 256;
-  const int64_t blocks = ((int64_t)g.n_trig + threads - 1) / threads;
-  hipLaunchKernelGGL(validate_kernel, dim3((unsigned)blocks), dim3(threads), 0, stream, g, trig, block_table,
-                     seq_lens, win_start, status);
+                           bool keep_kept, hipStream_t stream) {
+  if (g.n_trig == 0) return hipSuccess;
+  hipLaunchKernelGGL(validate_kernel, dim3((unsigned)g.n_trig), dim3(kValidateThreads), 0, stream, g, trig,
+                     block_table, seq_lens, win_start, status, keep_kept ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -19,7 +19,8 @@ HEADERS = [os.path.join(os.path.dirname(_PKG), "include", h)
 
 BF16, F32 = 0, 1
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_SCHED_MISMATCH, ERR_SCHED_NOMEM = 0, -1, -2, -3, -4, -5, -6
-SEQ_OK, SEQ_BAD_WINDOW, SEQ_BAD_PAGE, SEQ_DUP_TRIGGER, SEQ_BAD_INDEX, SEQ_BAD_KEPT = 0, 1, 2, 4, 8, 16
+SEQ_OK, SEQ_BAD_WINDOW, SEQ_BAD_PAGE, SEQ_DUP_TRIGGER, SEQ_BAD_INDEX, SEQ_BAD_KEPT, SEQ_DUP_PAGE = \
+    0, 1, 2, 4, 8, 16, 32
 MAX_COMPRESSIBLE = 4096
 REQ_WAITING, REQ_RUNNING, REQ_FINISHED = 0, 1, 2
 
@@ -109,6 +110,7 @@ _PAR = ctypes.POINTER(KaraParams)
 _SIGS = {
     "kara_status_string": (ctypes.c_char_p, [_I32]),
     "kara_abi_version": (_I32, []),
+    "kara_source_hash": (ctypes.c_char_p, []),
     "kara_last_hip_error": (ctypes.c_char_p, []),
     "kara_workspace_size": (_I32, [_PAR, _I32, _I32, ctypes.POINTER(ctypes.c_size_t)]),
     "kara_validate": (_I32, [_PAR, _I32, _VP, _VP, _VP, _VP, _VP, _VP]),
@@ -171,6 +173,13 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         fn = getattr(lib, name)
         fn.restype = res
         fn.argtypes = args
+    # refuse the in-tree library if it was built from other sources than the
+    # ones beside it
+    from .build import source_hash
+    built, here = lib.kara_source_hash().decode(), source_hash()
+    if os.path.abspath(path) == os.path.abspath(LIB_PATH) and built != here:
+        raise KaraError("load", ERR_HIP, f"{path} was built from other sources (library {built[:12]}, sources "
+                                         f"{here[:12]}); rebuild with python -m paper_2607_01237_amd.build")
     _lib = lib
     return lib
 

@@ -122,6 +122,8 @@ class Soak:
         self.freed = torch.empty((n, geom.max_blocks), dtype=torch.int32, device=device)
         self.n_freed = torch.empty(n, dtype=torch.int32, device=device)
         self.kept = torch.empty((L, n, self.Hkv, self.budget), dtype=torch.int32, device=device)
+        self.disc = torch.empty((L, n, self.Hkv, self.budget - c["chunk_budget"]), dtype=torch.int32,
+                                device=device)
         self.scores = torch.empty((L, n, self.Hkv, self.W - c["buffer"]), dtype=torch.float32, device=device)
         self.p0 = np.zeros(n, dtype=np.int32)
         self.reclaimed = 0
@@ -155,15 +157,22 @@ class Soak:
         if events:
             events[1].record()
 
-    def compress(self, events=None, want_scores=False):
-        """One compression event over every sequence and layer."""
+    def draw_queries(self):
+        """Fresh N(0,1) window queries for the next event; sets the window starts."""
         self.q.normal_(generator=self.gen)
         self.win_start.copy_(self.torch.from_numpy(self.p0))
+
+    def compress(self, events=None, want_scores=False, fresh_q=True):
+        """One compression event over every sequence and layer (with the
+        queries draw_queries() left when fresh_q is False)."""
+        if fresh_q:
+            self.draw_queries()
         if events:
             events[0].record()
         kara.compress_window(self.params, self.seqs, self.q, self.kp, self.vp, self.bt, self.lens, self.win_start,
                              True, self.status, self.ws, scores=self.scores if want_scores else None,
-                             kept=self.kept, freed=self.freed, n_freed=self.n_freed)
+                             discrete=self.disc if want_scores else None, kept=self.kept, freed=self.freed,
+                             n_freed=self.n_freed)
         if events:
             events[1].record()
 

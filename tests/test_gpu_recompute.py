@@ -3,12 +3,15 @@
 Attention (kara_recompute_attention): every output element against the
 oracle's fp64 causal attention over the same bf16 rows, within
 
-    |o_gpu - o_ora| <= 2^-8 (|o_ora| + 1)
+    |o_gpu - o_ora| <= u |o_ora| + 5 u sqrt(sum_j p_j^2 (v_j - o_ora)^2) + 2^-16
 
-The kernel rounds the softmax weights to bf16 (relative error up to
-u = 2^-8 each, random in sign) before the value product and rounds the
-output to bf16 (u|o|); with N(0,1) values the weighted sum of the weight
-errors stays well below u, and fp32 accumulation adds far less.
+with u = 2^-8 and p the oracle's softmax weights.  The kernel rounds each
+weight to bf16 (relative error up to u, random in sign) before the value
+product and normalises by the sum of the same rounded weights, so the
+error is sum_j p_j delta_j (v_j - o), whose standard deviation is at most
+u/sqrt(3) times the root above; the output store adds u|o|.  One key
+dropped or read twice among n moves o by about |v_j - o|/n, several times
+the bound at n = 2048 (a CPU test plants exactly that).
 
 Whole pass (kara_recompute_queries): each layer against the oracle's layer
 fed the GPU's own fp32 residual stream entering it.  bf16 keeps 8
@@ -69,7 +72,8 @@ def _setup(n_seqs, window, n_q, n_kv, d, bs, prefix, tail=(0, 8), seed=0):
     return geom, p, q, kp, vp, T(geom.trig), T(geom.block_table), T(geom.seq_lens), T(geom.win_start)
 
 
-def _oracle_attention(geom, p, q_h, kp_h, vp_h, t, rows=None):
+def _oracle_attention(geom, p, q_h, kp_h, vp_h, t, with_spread=False):
+    import kara_check as kc
     s = int(geom.trig[t])
     p0 = int(geom.win_start[s])
     W = p["window"]
@@ -77,7 +81,11 @@ def _oracle_attention(geom, p, q_h, kp_h, vp_h, t, rows=None):
     kr = rc.cache_rows(kp_h, geom.block_table[s], p0 + W, p["block_size"], to64)
     vr = rc.cache_rows(vp_h, geom.block_table[s], p0 + W, p["block_size"], to64)
     qs = to64(q_h[t])
-    return rc.causal_window_attention(qs, kr, vr, p0, 1.0 / math.sqrt(p["head_dim"]))
+    scale = 1.0 / math.sqrt(p["head_dim"])
+    o = rc.causal_window_attention(qs, kr, vr, p0, scale)
+    if not with_spread:
+        return o
+    return o, kc.attention_spread(qs, kr, vr, p0, scale, o)
 
 
 @pytest.mark.parametrize("window,n_q,n_kv,d,bs,prefix", [
@@ -102,14 +110,11 @@ def test_attention_parity(window, n_q, n_kv, d, bs, prefix):
     assert (status.cpu().numpy() == 0).all()
     got = to_f64(ki.raw_numpy(out), "bf16")
     q_h, kp_h, vp_h = ki.raw_numpy(q), ki.raw_numpy(kp), ki.raw_numpy(vp)
+    import kara_check as kc
     worst = 0.0
     for t in range(len(geom.trig)):
-        want = _oracle_attention(geom, p, q_h, kp_h, vp_h, t)
-        err = np.abs(got[t] - want)
-        tol = 2.0 ** -8 * (np.abs(want) + 1.0)
-        bad = err > tol
-        assert not bad.any(), f"trigger {t}: {bad.sum()} elements out of tolerance, max err {err.max():.3e}"
-        worst = max(worst, float(err.max()))
+        want, spread = _oracle_attention(geom, p, q_h, kp_h, vp_h, t, with_spread=True)
+        worst = max(worst, kc.check_attention(got[t], want, spread, f"trigger {t}"))
     print(f"[case] ok, max abs err {worst:.2e}", flush=True)
 
 

@@ -116,7 +116,9 @@ def test_compact_and_commit_bit_exact(case):
     status = torch.full((nt,), -1, dtype=torch.int32, device="cuda")
     freed = torch.full((nt, p["max_blocks_per_seq"]), -9, dtype=torch.int32, device="cuda")
     n_freed = torch.full((nt,), -9, dtype=torch.int32, device="cuda")
-    # compact layer by layer, then commit once (the per-layer calling pattern)
+    # an event starts with a status-resetting call; then compact layer by
+    # layer and commit once (the per-layer calling pattern)
+    kara.validate(case.params, case.trig, case.bt, case.seq_lens, case.win_start, status)
     kg = _dev(kept)
     for l in range(L):
         kara.compact_pages(case.params, case.trig, kg[l:l + 1].contiguous(), case.kp[l:l + 1], case.vp[l:l + 1],
@@ -139,6 +141,7 @@ def test_compact_rejects_bad_kept():
     kept[0, 1, 3, 5] = kept[0, 1, 3, 4]          # not strictly ascending in sequence 1
     before = [ki.raw_numpy(t) for t in c.kp]
     status = torch.full((nt,), -1, dtype=torch.int32, device="cuda")
+    kara.validate(c.params, c.trig, c.bt, c.seq_lens, c.win_start, status)
     kara.compact_pages(c.params, c.trig, _dev(kept), c.kp, c.vp, c.bt, c.seq_lens, c.win_start, status)
     torch.cuda.synchronize()
     st = status.cpu().numpy()
@@ -148,3 +151,54 @@ def test_compact_rejects_bad_kept():
     pos = np.arange(c.geom.win_start[s1], c.geom.seq_lens[s1])
     pg = c.geom.block_table[s1, pos // p["block_size"]]
     assert np.array_equal(after[pg, :, pos % p["block_size"]], before[0][pg, :, pos % p["block_size"]])
+
+
+def test_bad_kept_in_a_later_layer_stops_the_commit():
+    """Per-layer compaction: a bad kept set found in layer 1's call keeps the
+    sequence flagged through the commit, which then leaves its table,
+    length and freed list alone; the other sequence commits normally."""
+    import kara_check as kc
+    from paper_2607_01237_amd import kara
+    _need_gpu()
+    c = kc.setup(ki.workload("batch8", n_seqs=2, n_layers=2, window=256, budget=52))
+    p = c.p
+    nt, H, L = c.trig.numel(), p["n_kv_heads"], 2
+    kept = np.tile(np.arange(p["budget"], dtype=np.int32) * 2, (L, nt, H, 1))
+    kept[1, 1, 2, 7] = kept[1, 1, 2, 6]          # layer 1, sequence 1: not strictly ascending
+    bt0, sl0 = c.bt.cpu().numpy().copy(), c.seq_lens.cpu().numpy().copy()
+    status = torch.full((nt,), -1, dtype=torch.int32, device="cuda")
+    freed = torch.full((nt, p["max_blocks_per_seq"]), -9, dtype=torch.int32, device="cuda")
+    n_freed = torch.full((nt,), -9, dtype=torch.int32, device="cuda")
+    kara.validate(c.params, c.trig, c.bt, c.seq_lens, c.win_start, status)
+    kg = _dev(kept)
+    for l in range(L):
+        kara.compact_pages(c.params, c.trig, kg[l:l + 1].contiguous(), c.kp[l:l + 1], c.vp[l:l + 1], c.bt,
+                           c.seq_lens, c.win_start, status)
+    kara.commit_tables(c.params, c.trig, c.bt, c.seq_lens, c.win_start, freed, n_freed, status)
+    torch.cuda.synchronize()
+    st, bt, sl = status.cpu().numpy(), c.bt.cpu().numpy(), c.seq_lens.cpu().numpy()
+    fr, nf = freed.cpu().numpy(), n_freed.cpu().numpy()
+    s0, s1 = int(c.geom.trig[0]), int(c.geom.trig[1])
+    assert st[0] == 0 and st[1] == kara.SEQ_BAD_KEPT, st
+    assert np.array_equal(bt[s1], bt0[s1]) and sl[s1] == sl0[s1]
+    assert nf[1] == 0 and (fr[1] == -1).all()
+    N = p["window"] - p["buffer"]
+    assert sl[s0] == sl0[s0] - (N - p["budget"]) and nf[0] > 0
+
+
+def test_page_mapped_twice_is_flagged():
+    """A window whose block table maps one page at two blocks is flagged
+    KARA_SEQ_DUP_PAGE and left untouched; the others compress as the
+    oracle does (P1-P4)."""
+    import kara_check as kc
+    _need_gpu()
+    cfg = ki.workload("batch8", n_seqs=3, window=256, budget=52)
+    geom = ki.make_geometry(cfg)
+    bt = geom.block_table.copy()
+    s = int(geom.trig[1])
+    b0 = int(geom.win_start[s]) // geom.params()["block_size"]
+    bt[s, b0 + 3] = bt[s, b0 + 1]
+    case = kc.setup(cfg, block_table=bt)
+    rep, gpu = kc.full_check(case)
+    assert gpu["status"][1] == oracle.SEQ_DUP_PAGE and gpu["status"][0] == 0 and gpu["status"][2] == 0
+    print("dup page", rep)

@@ -155,6 +155,33 @@ def test_validation_flags_and_leaves_flagged_untouched():
     assert list(seq_lens) == [13, 13, 13, 5]
 
 
+
+def test_validation_flags_a_page_mapped_twice():
+    """R-PAGES: a page compaction writes may hold no other block of the same
+    sequence.  Sequence 0 maps page 5 twice inside its window; sequence 1 maps
+    its prefix page again at the window's last block; sequence 2 repeats a
+    page inside the prefix only, which compaction never writes; sequence 3
+    has an out-of-pool page and a duplicate (both bits)."""
+    p = _params(window=8, budget=3, num_pages=40, max_blocks_per_seq=6)
+    table = np.array([[0, 1, 5, 5, -1, -1],
+                      [6, 7, 8, 6, -1, -1],
+                      [9, 9, 10, 11, -1, -1],
+                      [12, 13, 99, 13, -1, -1]], dtype=np.int64)
+    seq_lens = np.array([13, 13, 16, 13])
+    win = np.array([4, 4, 8, 4])
+    st = oracle.validate(p, np.arange(4), table, seq_lens, win)
+    assert list(st) == [oracle.SEQ_DUP_PAGE, oracle.SEQ_DUP_PAGE, 0,
+                        oracle.SEQ_BAD_PAGE | oracle.SEQ_DUP_PAGE]
+    # flagged sequences are neither compacted nor committed
+    pool = _position_pool(p, np.where(table >= 40, 0, table), seq_lens)
+    before, tb = pool.copy(), table.copy()
+    scores = np.random.default_rng(2).random((1, 2, 1, 8)).astype(np.float32)
+    q = np.zeros((1, 2, 8, 1, 2), dtype=np.float32)
+    out = oracle.compress(p, [0, 1], q, [pool], [pool.copy()], table, seq_lens, win, score_override=scores)
+    assert list(out["status"]) == [oracle.SEQ_DUP_PAGE, oracle.SEQ_DUP_PAGE]
+    np.testing.assert_array_equal(pool, before)
+    np.testing.assert_array_equal(table, tb)
+
 def test_device_compaction_checker_on_the_oracle():
     """The all-units compaction check of the full-size GPU test, run on the
     CPU: it accepts the oracle's compaction and rejects a swapped row, a row
