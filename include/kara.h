@@ -77,7 +77,7 @@
 extern "C" {
 #endif
 
-#define KARA_ABI_VERSION 2
+#define KARA_ABI_VERSION 3
 
 /* Largest compressible region |W|-|U| one call supports. */
 #define KARA_MAX_COMPRESSIBLE 4096
@@ -92,7 +92,10 @@ typedef enum kara_status {
   KARA_ERR_INVALID_ARG = -1, /* a parameter is out of range or a pointer is NULL */
   KARA_ERR_UNSUPPORTED = -2, /* valid but not built (e.g. head_dim not 64/128) */
   KARA_ERR_WORKSPACE = -3,   /* workspace missing or smaller than kara_workspace_size() */
-  KARA_ERR_HIP = -4          /* the HIP runtime rejected a launch */
+  KARA_ERR_HIP = -4,         /* the HIP runtime rejected a launch */
+  KARA_ERR_SCRATCH_LIMIT = -7 /* kara_compress_window_noalloc: the call needs more than
+                                 KARA_NOALLOC_SCRATCH_BYTES of scratch, or the scratch
+                                 could not be resolved on the current device */
 } kara_status_t;
 
 /* Per-sequence device status bits. */
@@ -292,6 +295,38 @@ kara_status_t kara_compress_prefill(const kara_params_t* p, int32_t n_trig, cons
                                     float* scores, int32_t* discrete, int32_t* kept, int32_t* freed,
                                     int32_t* n_freed, int32_t* status, void* workspace,
                                     size_t workspace_bytes, void* stream);
+
+/*
+ * Allocation-free variant of kara_compress_window, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same arguments and results as
+ * kara_compress_window without the workspace: the partial column sums, and
+ * the scores and index sets the caller does not request, live in a static
+ * device array of KARA_NOALLOC_SCRATCH_BYTES that the library holds on every
+ * GPU it runs on until the process ends.  The call allocates nothing
+ * (no hipMalloc, hipFree or allocating library routine).
+ *
+ * Limit: the workspace kara_workspace_size() reports for (p, n_trig,
+ * n_layers) must fit in KARA_NOALLOC_SCRATCH_BYTES, else the call returns
+ * KARA_ERR_SCRATCH_LIMIT and enqueues nothing.  64 MiB holds about 1,700
+ * units of a 32/8-head, W = 1024 model with scores and index sets left to
+ * the library (38.4 KB each): 30 sequences x 7 layers, or one layer of 200
+ * sequences.  The array's device address is resolved once per
+ * device, on the first call with that device current.
+ *
+ * Every call on one GPU shares that GPU's array and leaves its contents
+ * there; nothing in it needs to start at zero.  Calls that overlap on one
+ * GPU (other streams or host threads without ordering) race on the array:
+ * the caller serialises them.
+ */
+#define KARA_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+kara_status_t kara_compress_window_noalloc(const kara_params_t* p, int32_t n_trig, const int32_t* trig,
+                                           int32_t n_layers, const void* q, void* const* k_pools,
+                                           void* const* v_pools, int32_t* block_table, int32_t* seq_lens,
+                                           const int32_t* win_start, int32_t commit, float* scores,
+                                           int32_t* discrete, int32_t* kept, int32_t* freed,
+                                           int32_t* n_freed, int32_t* status, void* stream);
 
 #ifdef __cplusplus
 }

@@ -149,6 +149,15 @@ hipError_t run_compact(const Geom& g, int n_layers, const int32_t* trig, const i
                           });
 }
 
+}  // namespace
+
+namespace kara {
+
+size_t compress_workspace_bytes(const Geom& g, int32_t n_layers) {
+  const ScorePlan sp = plan_score(g, (int64_t)n_layers * g.n_trig * g.n_win * g.Hkv);
+  return ws_layout(g, n_layers, sp).total;
+}
+
 // One compression event over n_win consecutive windows (stride W - U) of
 // each listed sequence: validation, scoring, selection, compaction and, if
 // asked, the metadata commit.
@@ -193,7 +202,7 @@ kara_status_t compress(const kara_params_t* p, int32_t n_trig, const int32_t* tr
   return hip_status(e);
 }
 
-}  // namespace
+}  // namespace kara
 
 extern "C" {
 
@@ -206,6 +215,9 @@ const char* kara_status_string(int32_t s) {
     case KARA_ERR_HIP: return "KARA_ERR_HIP: the HIP runtime rejected a launch";
     case -5: return "KARA_ERR_SCHED_MISMATCH: the device's freed pages differ from the scheduler's";
     case -6: return "KARA_ERR_SCHED_NOMEM: host memory for the scheduler could not be allocated";
+    case KARA_ERR_SCRATCH_LIMIT:
+      return "KARA_ERR_SCRATCH_LIMIT: the call needs more scratch than the allocation-free entry point holds "
+             "(KARA_NOALLOC_SCRATCH_BYTES per device), or its scratch could not be resolved on this device";
     default: return "unknown kara status";
   }
 }

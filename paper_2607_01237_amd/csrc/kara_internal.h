@@ -77,6 +77,16 @@ hipError_t launch_commit(const Geom& g, const int32_t* trig, int32_t* block_tabl
                          int32_t* seq_lens, const int32_t* win_start, int32_t* freed,
                          int32_t* n_freed, const int32_t* status, hipStream_t stream);
 
+// One compression event (kara_api.cpp): the body of kara_compress_window
+// (n_win = 1) and kara_compress_prefill, workspace supplied by the caller.
+kara_status_t compress(const kara_params_t* p, int32_t n_trig, const int32_t* trig, int32_t n_win,
+                       int32_t n_layers, const void* q, void* const* k_pools, void* const* v_pools,
+                       int32_t* block_table, int32_t* seq_lens, const int32_t* win_start, int32_t commit,
+                       float* scores, int32_t* discrete, int32_t* kept, int32_t* freed, int32_t* n_freed,
+                       int32_t* status, void* workspace, size_t workspace_bytes, void* stream);
+// Workspace bytes compress() needs for g (g.n_trig, g.n_win set) and n_layers.
+size_t compress_workspace_bytes(const Geom& g, int32_t n_layers);
+
 // Window recompute pass (kara_attn.hip, kara_recompute_ops.hip).
 // Validation of the listed sequences for the recompute pass: index, duplicate,
 // window inside the sequence, pages of [0, p0 + W) inside the pool.

@@ -19,6 +19,8 @@ HEADERS = [os.path.join(os.path.dirname(_PKG), "include", h)
 
 BF16, F32 = 0, 1
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_SCHED_MISMATCH, ERR_SCHED_NOMEM = 0, -1, -2, -3, -4, -5, -6
+ERR_SCRATCH_LIMIT = -7
+NOALLOC_SCRATCH_BYTES = 64 << 20      # KARA_NOALLOC_SCRATCH_BYTES
 SEQ_OK, SEQ_BAD_WINDOW, SEQ_BAD_PAGE, SEQ_DUP_TRIGGER, SEQ_BAD_INDEX, SEQ_BAD_KEPT, SEQ_DUP_PAGE = \
     0, 1, 2, 4, 8, 16, 32
 MAX_COMPRESSIBLE = 4096
@@ -122,6 +124,8 @@ _SIGS = {
     "kara_commit_tables": (_I32, [_PAR, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     "kara_compress_window": (_I32, [_PAR, _I32, _VP, _I32, _VP, _PP, _PP, _VP, _VP, _VP, _I32, _VP, _VP,
                                     _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP]),
+    "kara_compress_window_noalloc": (_I32, [_PAR, _I32, _VP, _I32, _VP, _PP, _PP, _VP, _VP, _VP, _I32, _VP, _VP,
+                                            _VP, _VP, _VP, _VP, _VP]),
     "kara_compress_prefill": (_I32, [_PAR, _I32, _VP, _I32, _I32, _VP, _PP, _PP, _VP, _VP, _VP, _I32, _VP, _VP,
                                      _VP, _VP, _VP, _VP, _VP, ctypes.c_size_t, _VP]),
     "kara_harness_kv_append": (_I32, [_PAR, _I32, _VP, _I32, _I32, _VP, _VP, _PP, _PP, _VP, _VP, _VP, _VP]),
@@ -365,6 +369,17 @@ def compress_window(p, trig, q, k_pools, v_pools, block_table, seq_lens, win_sta
         workspace.numel() * workspace.element_size() if workspace is not None else 0, _stream(stream)))
 
 
+
+def compress_window_noalloc(p, trig, q, k_pools, v_pools, block_table, seq_lens, win_start, commit, status,
+                            scores=None, discrete=None, kept=None, freed=None, n_freed=None, stream=None):
+    """kara_compress_window without a workspace: the library's static
+    per-device scratch (NOALLOC_SCRATCH_BYTES) holds it."""
+    _compress_checks(p, trig, 1, q, k_pools, v_pools, block_table, seq_lens, win_start, status, scores, discrete,
+                     kept, freed, n_freed)
+    _check("kara_compress_window_noalloc", load().kara_compress_window_noalloc(
+        ctypes.byref(p), trig.numel(), _ptr(trig), len(k_pools), _ptr(q), _ptr_array(k_pools),
+        _ptr_array(v_pools), _ptr(block_table), _ptr(seq_lens), _ptr(win_start), int(bool(commit)),
+        _ptr(scores), _ptr(discrete), _ptr(kept), _ptr(freed), _ptr(n_freed), _ptr(status), _stream(stream)))
 
 def compress_prefill(p, trig, n_windows, q, k_pools, v_pools, block_table, seq_lens, win_start, commit, status,
                      workspace, scores=None, discrete=None, kept=None, freed=None, n_freed=None, stream=None):

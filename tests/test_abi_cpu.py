@@ -29,8 +29,8 @@ def good_params(**kw):
 
 def test_exports_every_declared_function(lib):
     names = kara.header_functions()
-    # 13 in kara.h, 3 in kara_harness.h, 9 in kara_sched.h, 3 in kara_recompute.h
-    assert len(names) == 28, names
+    # 14 in kara.h, 3 in kara_harness.h, 9 in kara_sched.h, 3 in kara_recompute.h
+    assert len(names) == 29, names
     for n in names:
         assert hasattr(lib, n), n
 
@@ -41,8 +41,8 @@ def test_library_is_built_from_these_sources(lib):
 
 
 def test_version_and_status_strings(lib):
-    assert kara.abi_version() == 2
-    for code in (0, -1, -2, -3, -4, -5, -6):
+    assert kara.abi_version() == 3
+    for code in (0, -1, -2, -3, -4, -5, -6, -7):
         assert kara.status_string(code).startswith("KARA_")
     assert "unknown" in kara.status_string(12345)
     # nothing has failed on this thread: no HIP call is made to say so
@@ -121,6 +121,26 @@ def test_workspace_checked_before_launch(lib):
     rc = lib.kara_compress_window(ctypes.byref(p), 2, fake, 1, fake, pools, pools, fake, fake, fake, 1, None,
                                   None, None, fake, fake, fake, fake, 16, None)
     assert rc == kara.ERR_WORKSPACE
+
+
+def test_noalloc_rejects_calls_past_its_scratch(lib):
+    """The allocation-free entry point refuses, before touching any pointer,
+    a call whose workspace would not fit its static scratch; empty calls
+    succeed."""
+    p = good_params()
+    fake = ctypes.c_void_p(0x1000)   # never dereferenced
+    pools = (ctypes.c_void_p * 40)(*([0x1000] * 40))
+    need = kara.workspace_size(p, 64, 40)
+    assert need > kara.NOALLOC_SCRATCH_BYTES
+    rc = lib.kara_compress_window_noalloc(ctypes.byref(p), 64, fake, 40, fake, pools, pools, fake, fake, fake, 1,
+                                          None, None, None, fake, fake, fake, None)
+    assert rc == kara.ERR_SCRATCH_LIMIT
+    assert "KARA_NOALLOC_SCRATCH_BYTES" in kara.status_string(rc)
+    assert lib.kara_compress_window_noalloc(ctypes.byref(p), 0, None, 1, None, None, None, None, None, None, 1,
+                                            None, None, None, None, None, None, None) == kara.OK
+    # one layer of 200 such sequences fits, as the header says
+    assert kara.workspace_size(p, 200, 1) <= kara.NOALLOC_SCRATCH_BYTES
+    assert kara.workspace_size(good_params(), 30, 7) <= kara.NOALLOC_SCRATCH_BYTES
 
 
 def test_harness_checks_before_launch(lib):

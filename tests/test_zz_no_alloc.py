@@ -1,0 +1,125 @@
+"""kara_compress_window_noalloc against kara_compress_window.
+
+The allocation-free entry point runs the same kernels with its workspace in
+the library's static per-device scratch.  Two calls in a row, the second on
+a smaller input (the scratch then holds the first call's contents): each
+must give the same scores, index sets, status, freed lists, block tables,
+lengths and compacted K/V as kara_compress_window on an identical copy of
+its inputs, bit for bit.  A call past the scratch limit is refused with
+KARA_ERR_SCRATCH_LIMIT and changes nothing.
+"""
+import numpy as np
+import pytest
+
+import kara_inputs as ki
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _inputs(cfg, dev):
+    geom = ki.make_geometry(cfg)
+    L = cfg["n_layers"]
+    q = torch.stack([ki.make_queries(geom, l, dev) for l in range(L)]).contiguous()
+    pools = [ki.make_pools(geom, l, dev) for l in range(L)]
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    return geom, dict(q=q, kp=[x[0] for x in pools], vp=[x[1] for x in pools], bt=T(geom.block_table),
+                      lens=T(geom.seq_lens), ws=T(geom.win_start), trig=T(geom.trig))
+
+
+def _clone(x):
+    return dict(q=x["q"], kp=[t.clone() for t in x["kp"]], vp=[t.clone() for t in x["vp"]], bt=x["bt"].clone(),
+                lens=x["lens"].clone(), ws=x["ws"], trig=x["trig"])
+
+
+def _outputs(p, L, nt, dev):
+    H, N = p["n_kv_heads"], p["window"] - p["buffer"]
+    f = lambda shape, dt, v: torch.full(shape, v, dtype=dt, device=dev)
+    return dict(scores=f((L, nt, H, N), torch.float32, float("nan")),
+                discrete=f((L, nt, H, p["budget"] - p["chunk_budget"]), torch.int32, -7),
+                kept=f((L, nt, H, p["budget"]), torch.int32, -7),
+                freed=f((nt, p["max_blocks_per_seq"]), torch.int32, -7),
+                n_freed=f((nt,), torch.int32, -7), status=f((nt,), torch.int32, -7))
+
+
+def _same(a, b):
+    return torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a,
+                       b.view(torch.int16) if b.dtype == torch.bfloat16 else b)
+
+
+def _compare_once(cfg, dev, tag):
+    from paper_2607_01237_amd import kara
+    geom, x = _inputs(cfg, dev)
+    p = geom.params()
+    params = kara.make_params(p, geom.block_table.shape[0])
+    L, nt = cfg["n_layers"], len(geom.trig)
+    need = kara.workspace_size(params, nt, L)
+    assert need <= kara.NOALLOC_SCRATCH_BYTES
+    print(f"\n[case] no-alloc {tag}: {nt} seqs x {L} layers, W={p['window']}, workspace {need / 2**20:.1f} MiB",
+          flush=True)
+    a, b = _clone(x), _clone(x)
+    oa, ob = _outputs(p, L, nt, dev), _outputs(p, L, nt, dev)
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    kara.compress_window(params, a["trig"], a["q"], a["kp"], a["vp"], a["bt"], a["lens"], a["ws"], True,
+                         oa["status"], ws, scores=oa["scores"], discrete=oa["discrete"], kept=oa["kept"],
+                         freed=oa["freed"], n_freed=oa["n_freed"])
+    kara.compress_window_noalloc(params, b["trig"], b["q"], b["kp"], b["vp"], b["bt"], b["lens"], b["ws"], True,
+                                 ob["status"], scores=ob["scores"], discrete=ob["discrete"], kept=ob["kept"],
+                                 freed=ob["freed"], n_freed=ob["n_freed"])
+    torch.cuda.synchronize()
+    assert (oa["status"].cpu().numpy() == 0).all()
+    for k in oa:
+        assert _same(oa[k], ob[k]), f"{tag}: {k} differs"
+    for k in ("bt", "lens"):
+        assert _same(a[k], b[k]), f"{tag}: {k} differs"
+    for l in range(L):
+        assert _same(a["kp"][l], b["kp"][l]) and _same(a["vp"][l], b["vp"][l]), f"{tag}: pools of layer {l}"
+    # the no-alloc call with scores and index sets left to the library too
+    c, oc = _clone(x), _outputs(p, L, nt, dev)
+    kara.compress_window_noalloc(params, c["trig"], c["q"], c["kp"], c["vp"], c["bt"], c["lens"], c["ws"], True,
+                                 oc["status"], freed=oc["freed"], n_freed=oc["n_freed"])
+    torch.cuda.synchronize()
+    assert _same(oa["freed"], oc["freed"]) and _same(a["lens"], c["lens"])
+    for l in range(L):
+        assert _same(a["kp"][l], c["kp"][l]) and _same(a["vp"][l], c["vp"][l]), f"{tag}: pools of layer {l} (bare)"
+    print(f"[case] no-alloc {tag}: identical", flush=True)
+
+
+def test_noalloc_matches_compress_window_twice():
+    _need_gpu()
+    dev = torch.device("cuda:0")
+    # first the larger call, then a smaller one over the scratch it left
+    _compare_once(ki.workload("qwen14b", n_seqs=6, n_layers=3, n_q_heads=40, n_kv_heads=8, window=1024,
+                              budget=205, prefix=(100, 900), num_pages=None), dev, "6 x 3, W=1024")
+    _compare_once(ki.workload("batch8", n_seqs=3, n_layers=1, window=256, budget=52), dev, "3 x 1, W=256")
+
+
+def test_noalloc_refuses_past_its_scratch():
+    from paper_2607_01237_amd import kara
+    _need_gpu()
+    dev = torch.device("cuda:0")
+    cfg = ki.workload("batch8", n_seqs=8, n_layers=40, window=1024, budget=205)
+    geom = ki.make_geometry(cfg)
+    p = geom.params()
+    params = kara.make_params(p, geom.block_table.shape[0])
+    nt, L = len(geom.trig), cfg["n_layers"]
+    assert kara.workspace_size(params, nt, L) > kara.NOALLOC_SCRATCH_BYTES
+    # no inputs are touched before the size check: small stand-ins suffice
+    small = torch.zeros(1, dtype=torch.bfloat16, device=dev)
+    pools = [small] * L
+    i32 = lambda n: torch.zeros(n, dtype=torch.int32, device=dev)
+    status = i32(nt).fill_(-7)
+    lib = kara.load()
+    import ctypes
+    rc = lib.kara_compress_window_noalloc(
+        ctypes.byref(params), nt, kara._ptr(i32(nt)), L, kara._ptr(small), kara._ptr_array(pools),
+        kara._ptr_array(pools), kara._ptr(i32(1)), kara._ptr(i32(1)), kara._ptr(i32(1)), 1, None, None, None,
+        kara._ptr(i32(1)), kara._ptr(i32(1)), kara._ptr(status), None)
+    torch.cuda.synchronize()
+    assert rc == kara.ERR_SCRATCH_LIMIT
+    assert (status.cpu().numpy() == -7).all()
