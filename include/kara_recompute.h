@@ -24,19 +24,27 @@
  * on the queries (cached keys carry theirs), SwiGLU feed-forward, no biases.
  *
  * Conventions are those of kara.h: device pointers owned by the caller,
- * nothing allocated, nothing synchronised, argument errors as return codes
- * with nothing enqueued, per-sequence problems in status[t] (KARA_SEQ_*):
- * index out of range, listed twice, window past the sequence end
- * (p0 + window > seq_len), or a page of [0, p0 + window) outside the pool.
- * A flagged sequence's attention output and scoring queries are left
- * unwritten; kara_recompute_queries runs the matrix products over every
- * listed row, so a flagged sequence's hidden_out rows are unspecified.  bf16 only
+ * nothing synchronised, argument errors as return codes with nothing
+ * enqueued, per-sequence problems in status[t] (KARA_SEQ_*): index out of
+ * range, listed twice, window past the sequence end (p0 + window >
+ * seq_len), or a page of [0, p0 + window) outside the pool.  A flagged
+ * sequence's attention output and scoring queries are left unwritten;
+ * kara_recompute_queries runs the matrix products over every listed row, so
+ * a flagged sequence's hidden_out rows are unspecified.  bf16 only
  * (params.dtype = KARA_BF16, else KARA_ERR_UNSUPPORTED), head_dim 64 or 128.
- * Device arrays are 16-byte aligned.  kara_recompute_queries creates one
- * rocBLAS handle per device on its first call there; rocBLAS allocates that
- * handle's own workspace.  Each call binds that handle to its stream, so
- * calls on one device from several host threads at once must be serialised
- * by the caller.
+ * Device arrays are 16-byte aligned.
+ *
+ * Allocation.  The matrix products run on rocBLAS.  Their scratch is a
+ * 32 MiB slice of the caller's workspace, handed to rocBLAS
+ * (rocblas_set_workspace) after a size query has confirmed the products fit
+ * in it (else KARA_ERR_WORKSPACE), so rocBLAS allocates no workspace of its
+ * own.  The one thing the library creates on this path is the rocBLAS
+ * handle: kara_recompute_queries makes one per device on its first call
+ * there (rocblas_create_handle: rocBLAS's host state and whatever device
+ * memory the handle takes for itself) and keeps it until the process ends;
+ * later calls allocate nothing.  Each call binds that handle to its stream
+ * and workspace, so calls on one device from several host threads at once
+ * must be serialised by the caller.
  *
  * Layouts (row-major)
  *   q, out (attention)  [n_trig][window][n_q_heads][head_dim] bf16

@@ -28,8 +28,13 @@ bool model_ok(const kara_model_t* m) {
 }
 
 struct RecomputeWs {
-  size_t x, qraw, attn, gate, up, total;
+  size_t x, qraw, attn, gate, up, blas, total;
 };
+
+// Scratch handed to rocBLAS for the products (rocblas_set_workspace), so it
+// allocates none of its own; each call checks with a size query that its
+// products fit.
+constexpr size_t kBlasWorkspace = (size_t)32 << 20;
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
@@ -47,12 +52,14 @@ RecomputeWs recompute_ws(const Geom& g, const kara_model_t& m, int32_t n_trig) {
   off += align256(T * m.ffn * 2);
   w.up = off;
   off += align256(T * m.ffn * 2);
+  w.blas = off;
+  off += kBlasWorkspace;
   w.total = off;
   return w;
 }
 
-// One rocBLAS handle per device, created on first use (rocBLAS then owns
-// its own workspace on that device).
+// One rocBLAS handle per device, created on first use; each call then points
+// it at the caller's workspace slice.
 constexpr int kMaxDevices = 64;
 rocblas_handle g_handles[kMaxDevices];
 std::mutex g_handle_mutex;
@@ -146,6 +153,20 @@ kara_status_t kara_recompute_queries(const kara_params_t* p, const kara_model_t*
   void* attn = ws + wl.attn;
   void* gate = ws + wl.gate;
   void* up = ws + wl.up;
+  // the products' scratch is the caller's: size the products (a size query
+  // launches nothing), then hand rocBLAS the slice
+  {
+    const kara_layer_weights_t& w = weights[0];
+    if (rocblas_start_device_memory_size_query(h) != rocblas_status_success) return KARA_ERR_HIP;
+    (void)gemm(h, T, HD, m->hidden, x, w.w_q, qraw, false);
+    (void)gemm(h, T, m->hidden, HD, attn, w.w_o, hidden_out, true);
+    (void)gemm(h, T, m->ffn, m->hidden, x, w.w_gate, gate, false);
+    (void)gemm(h, T, m->hidden, m->ffn, gate, w.w_down, hidden_out, true);
+    size_t need = 0;
+    if (rocblas_stop_device_memory_size_query(h, &need) != rocblas_status_success) return KARA_ERR_HIP;
+    if (need > kBlasWorkspace) return KARA_ERR_WORKSPACE;
+    if (rocblas_set_workspace(h, ws + wl.blas, kBlasWorkspace) != rocblas_status_success) return KARA_ERR_HIP;
+  }
   const size_t q_layer = (size_t)T * HD * 2;
 
   hipError_t e = launch_recompute_validate(g, trig, block_table, seq_lens, win_start, status, s);

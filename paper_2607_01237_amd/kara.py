@@ -13,7 +13,9 @@ import os
 import re
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libkara.so")
+# the in-tree library; KARA_LIBRARY names another build of the same sources
+# (the host-sanitized one the CPU tests load)
+LIB_PATH = os.environ.get("KARA_LIBRARY") or os.path.join(_PKG, "libkara.so")
 HEADERS = [os.path.join(os.path.dirname(_PKG), "include", h)
            for h in ("kara.h", "kara_harness.h", "kara_sched.h", "kara_recompute.h")]
 
@@ -177,11 +179,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         fn = getattr(lib, name)
         fn.restype = res
         fn.argtypes = args
-    # refuse the in-tree library if it was built from other sources than the
-    # ones beside it
+    # refuse a library built from other sources than the ones beside it
     from .build import source_hash
     built, here = lib.kara_source_hash().decode(), source_hash()
-    if os.path.abspath(path) == os.path.abspath(LIB_PATH) and built != here:
+    if built != here:
         raise KaraError("load", ERR_HIP, f"{path} was built from other sources (library {built[:12]}, sources "
                                          f"{here[:12]}); rebuild with python -m paper_2607_01237_amd.build")
     _lib = lib

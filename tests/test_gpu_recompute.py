@@ -230,6 +230,14 @@ def test_recompute_pass_layers(window, n_q, n_kv, d, D, F, bs):
     for l in range(L):
         assert torch.equal(q_all[l].view(torch.int16), q_layers[l].view(torch.int16)), f"layer {l} queries"
     assert torch.equal(h_all, h)
+    # after the first call on the device, calls allocate nothing: the device's
+    # free memory is unchanged across another full call
+    torch.cuda.synchronize()
+    free0, _ = torch.cuda.mem_get_info()
+    kara.recompute_queries(params, model, trig, wts, h0, h_all, kp, vp, bt, lens, ws, rope_pos0, q_all, status, wsp)
+    torch.cuda.synchronize()
+    free1, _ = torch.cuda.mem_get_info()
+    assert free1 == free0, f"a recompute call took {free0 - free1} bytes of device memory"
     print("[case] ok", flush=True)
 
 
