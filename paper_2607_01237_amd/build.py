@@ -38,6 +38,10 @@ FLAGS = [
 # registers (56 VGPRs instead of 126, no scratch either way).
 FILE_FLAGS = {
     "kara_select.hip": ["-mllvm", "-amdgpu-promote-alloca-to-vector-limit=256"],
+    # scoring: MFMA results in ordinary VGPRs, read directly by the vector
+    # instructions; the accumulation registers hold the single-sweep
+    # kernel's stored weights
+    "kara_score.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 # rocBLAS runs the recompute pass's plain matrix products
 LINK_LIBS = ["-L/opt/rocm/lib", "-lrocblas"]

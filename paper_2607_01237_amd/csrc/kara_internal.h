@@ -52,6 +52,7 @@ hipError_t launch_validate(const Geom& g, const int32_t* trig, const int32_t* bl
 struct ScorePlan {
   int rows_wg;          // query rows per workgroup
   int n_splits;         // row splits (workgroups) per unit
+  int single_nt;        // key tiles per wave of the single-sweep kernel; 0: two sweeps
 };
 ScorePlan plan_score(const Geom& g, int64_t n_units);
 hipError_t launch_score(const Geom& g, const ScorePlan& sp, int n_layers, const void* q,

@@ -2,7 +2,13 @@
 // per (sequence, layer, KV head), all G query heads of the group acting as
 // queries of their KV head.
 //
-// Two sweeps over the keys per workgroup.  A workgroup of 8 waves owns 128*RT
+// Two kernels.  score1_kernel (bf16, d = 128, 512 < N <= 2048, the shapes
+// of the Qwen3-shaped workloads) forms and exponentiates every logit once,
+// holding each row block's weights in fp16 until the block's row sums are
+// known; it is described where it is defined.  score_kernel serves every
+// other shape with two sweeps over the keys:
+//
+// A workgroup of 8 waves owns 128*RT
 // query rows of one unit (16*RT rows per wave, held as MFMA operands in
 // registers for the whole kernel) and streams the unit's N keys through an
 // LDS ring, 64 keys per chunk, twice:
@@ -11,19 +17,18 @@
 // Every wave sees every key of its own rows, so the row statistics need no
 // exchange between waves.  Recomputing the logits doubles the matrix work
 // but keeps nothing per logit between the sweeps, so the rows sharing one
-// read of the keys (512 for bf16) are limited by the operand registers only;
-// a single sweep would have to hold every logit of its rows in registers and
-// re-read all keys for every 32 rows.  Keys reach LDS by direct global->LDS
+// read of the keys (512 for bf16) are limited by the operand registers only.
+// Keys reach LDS by direct global->LDS
 // copies, so no register is spent on staging and the copies of later chunks
 // overlap the matrix and exponential work of the current one.
 //
 // Column sums of a chunk are reduced within each wave in a fixed lane order,
 // then across the 8 waves in wave order into a per-workgroup row in LDS.
-// Each workgroup writes one partial sum per row split and a second kernel
-// adds them in split order.  (Handing the sum to the last split to finish
-// would need a device-scope release/acquire, which on this multi-XCD part
-// writes back and invalidates the whole L2 of the XCD every time.)  No
-// floating-point atomics, so the scores are bit-reproducible.
+// Each workgroup (of either kernel) writes one partial sum per row split and
+// a second kernel adds them in split order.  (Handing the sum to the last
+// split to finish would need a device-scope release/acquire, which on this
+// multi-XCD part writes back and invalidates the whole L2 of the XCD every
+// time.)  No floating-point atomics, so the scores are bit-reproducible.
 #include <type_traits>
 
 #include "kara_internal.h"
@@ -583,6 +588,478 @@ __global__ __launch_bounds__(256) void split_sum_kernel(const float* __restrict_
   scores[u * (int64_t)N + j] = v;
 }
 
+// ---------------------------------------------------------------------------
+// Single-sweep scoring (bf16, d = 128, up to 2048 compressible keys).
+//
+// Every logit is formed and exponentiated once.  A workgroup of 4 waves, one
+// per SIMD, takes a unit's query rows 64 at a time (a row block); within a
+// block wave w owns the keys of tiles [w*ntw, (w+1)*ntw) (16 keys a tile)
+// against all 64 rows, so its tiles' weights e = 2^(x - m) fit in its
+// accumulation registers as fp16 (64 rows x 512 keys = 256 registers).  The
+// reference m of a row is shared by the four waves: the maximum of their
+// first tiles' logits less kS1Headroom, exchanged once per block through
+// LDS.  When the row sums are known, the weights 1/L (one per row, the same
+// for every wave since m is shared) are applied by fp16 MFMAs of the stored
+// values, 32 rows at a time, which sums each key's column.  The keys of a
+// wave stream through its own LDS ring by direct global->LDS copies, the
+// same keys for every block of the unit, so the ring runs on across blocks
+// and no workgroup barrier guards it; the next block's queries are copied
+// into LDS during the current block.
+//
+// Precision.  e is rounded once to fp16 (relative error 2^-11, or 2^-25
+// absolute below fp16's normal range); the row weight is carried as an
+// fp16 pair (hi + lo) scaled by 2^21, so it loses nothing that matters; all
+// sums are fp32.  With m = (first-tile maximum) - 6 the top first-tile term
+// is 64, so a term of fp16's subnormal range contributes at most 2^-31 to a
+// probability.  A row whose later logits rise more than about 10 log2 units
+// above its first tiles' maximum would overflow fp16: any wave's row sum
+// reaching 65504 (which every overflowing term would exceed) sends the block
+// through once more with m = (exact row maximum) - 6, where no term exceeds
+// 64 and no wave sum 64 * 512.
+// ---------------------------------------------------------------------------
+constexpr int kS1Threads = 256;
+constexpr int kS1Waves = kS1Threads / 64;
+constexpr int kS1Rows = 64;                // query rows per block: 4 row tiles per wave
+constexpr int kS1Stages = 8;               // key tiles in each wave's LDS ring
+constexpr int kS1Ahead = kS1Stages - 1;    // tiles copied ahead of the one being read
+constexpr int kS1QIt = 2;                  // iteration that copies the next block's queries
+constexpr int kS1RowBytes = 256;           // one bf16 row of 128
+constexpr int kS1TileBytes = 16 * kS1RowBytes;
+constexpr float kS1Headroom = 6.f;
+constexpr float kF16Max = 65504.f;
+constexpr float kS1WScale = 2097152.f;     // 2^21: row weights 1/L, L in [64, 2^18], as fp16
+constexpr int kS1BlocksPerSplit = 8;       // row blocks per workgroup (512 rows, as the two-sweep kernel)
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef float float2v __attribute__((ext_vector_type(2)));
+
+struct Score1Args {
+  ScoreArgs s;
+  int ntw;          // key tiles per wave
+  int bps;          // row blocks per split
+};
+
+// the 16-byte chunk swizzle of a 256-byte row in LDS (conflict-free for the
+// operand reads: row's two low bits moved to the top)
+__device__ __forceinline__ int s1_swz(int row) { return ((row & 3) << 2) | ((row >> 2) & 3); }
+
+// Reductions over the 16 lanes of a row by DPP butterflies (quad swaps,
+// then half-row and row mirrors).  Every lane ends with the same value:
+// each step combines two equal partial results, in either order.
+template <class Op>
+__device__ __forceinline__ float dpp_reduce16(float v, Op op) {
+  v = op(v, __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false)));
+  v = op(v, __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, false)));
+  v = op(v, __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x141, 0xF, 0xF, false)));
+  v = op(v, __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x140, 0xF, 0xF, false)));
+  return v;
+}
+__device__ __forceinline__ float dpp_max16(float v) {
+  return dpp_reduce16(v, [](float x, float y) { return fmaxf(x, y); });
+}
+__device__ __forceinline__ float dpp_sum16(float v) {
+  return dpp_reduce16(v, [](float x, float y) { return x + y; });
+}
+
+// Direct global->LDS copy of 16 bytes per lane to LDS address base + off
+// (base wave-uniform, off a constant): lane i's bytes land at base + off +
+// 16 i.  M0 is formed by one scalar add and restored.
+template <int OFF>
+__device__ __forceinline__ void copy16_at(const void* gp, uint32_t base) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_add_u32 m0, %2, %3\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(gp), "s"(base), "n"(OFF)
+      : "memory", "scc");
+}
+
+// a packed weight pair into an accumulation register (it is only read by MFMAs)
+__device__ __forceinline__ uint32_t s1_to_agpr(uint32_t x) {
+  uint32_t r;
+  asm volatile("v_accvgpr_write_b32 %0, %1" : "=a"(r) : "v"(x));
+  return r;
+}
+
+__device__ __forceinline__ uint32_t s1_pack(float a, float b) {
+  const float2v v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, f16x2));   // round to nearest
+}
+
+// Calls f(std::integral_constant<int, I>) for I = B..E-1: a loop whose
+// index is a compile-time constant in every copy of the body.
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
+// FULL: every wave's NT tiles hold keys below N (N = 64 * NT), so no tile
+// is skipped or masked.
+template <int NT, bool FULL>
+__global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void score1_kernel(Score1Args aa) {
+  static_assert(NT % kS1Stages == 0 && NT % 4 == 0, "tiles per wave: a multiple of the ring and of 4");
+  constexpr int D = kS1Ahead;
+  constexpr int S = kS1Stages;
+  const ScoreArgs& a = aa.s;
+  __shared__ __attribute__((aligned(16))) char kring[kS1Waves][S][kS1TileBytes];
+  __shared__ __attribute__((aligned(16))) char qbuf[kS1Rows * kS1RowBytes];
+  // byte offset / 16 of key j's row in the K pool; entries past N repeat key 0
+  __shared__ uint32_t key_off[kS1Waves * NT * 16];
+  __shared__ __attribute__((aligned(16))) float smax[kS1Waves][kS1Rows];
+  __shared__ __attribute__((aligned(16))) float ssum[kS1Waves][kS1Rows];
+
+  const Geom& g = a.g;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int gq = lane >> 4;
+  const int li = lane & 15;
+
+  // the row splits of one unit run together on one XCD (its L2 keeps the keys)
+  int64_t bid = blockIdx.x;
+  if ((a.n_blocks & 7) == 0) bid = (bid & 7) * (a.n_blocks >> 3) + (bid >> 3);
+  const int64_t u = bid / a.n_splits;
+  const int split = (int)(bid % a.n_splits);
+  const int h = (int)(u % g.Hkv);
+  const int tw = (int)((u / g.Hkv) % ((int64_t)g.n_trig * g.n_win));
+  const int t = tw / g.n_win;
+  const int wi = tw - t * g.n_win;
+  const int l = (int)(u / ((int64_t)g.Hkv * g.n_trig * g.n_win));
+  const int N = g.N;
+  float* out = a.n_splits == 1 ? a.scores + u * (int64_t)N : a.partials + (u * a.n_splits + split) * (int64_t)N;
+  if (a.status[t] != 0) {
+    for (int j = tid; j < N; j += kS1Threads) out[j] = 0.f;
+    return;
+  }
+  const int s = a.trig[t];
+  const int p0 = a.win_start[s] + wi * N;
+  const char* kpool = (const char*)a.k.p[l];
+  const char* qunit = a.q + (((int64_t)l * g.n_trig + t) * g.n_win + wi) * g.Wq * g.Hq * (int64_t)kS1RowBytes;
+  const int R = g.G * g.Wq;
+  const float c = g.scale * kLog2e;
+  const int nblk = (R + kS1Rows - 1) / kS1Rows;
+  const int b0 = split * aa.bps;
+  const int b1 = min(nblk, b0 + aa.bps);
+  const int ntw = aa.ntw;
+  const int T = (N + 15) / 16;
+  const int wt0 = wave * ntw;                             // this wave's first tile
+  const int nvalid = FULL ? NT : max(0, min(ntw, T - wt0));   // its tiles holding a key < N
+
+  {
+    const int32_t* row_pages = a.bt + (int64_t)s * g.max_blocks;
+    for (int j = tid; j < kS1Waves * NT * 16; j += kS1Threads) {
+      const int pos = p0 + (j < N ? j : 0);
+      const uint64_t row = ((uint64_t)row_pages[pos / g.bs] * g.Hkv + h) * g.bs + pos % g.bs;
+      key_off[j] = (uint32_t)(row * (kS1RowBytes / 16));
+    }
+  }
+  lds_barrier();
+
+  // ---- copies.  Copy r of a tile fills slots r*64 + lane: key row kr =
+  // 4r + gq, stored chunk li holding the row's chunk li ^ swz(kr).
+  int kchunk[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) kchunk[r] = (li ^ s1_swz(4 * r + gq)) * 16;
+  uint32_t coff[4];
+  auto read_offsets = [&](int tile) __attribute__((always_inline)) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) coff[r] = key_off[(wt0 + tile) * 16 + 4 * r + gq];
+  };
+  const uint32_t ring_base = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)&kring[wave][0][0]);
+  const uint32_t qbuf_base = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)&qbuf[16 * wave * kS1RowBytes]);
+  auto issue_k = [&](auto stage_c) __attribute__((always_inline)) {
+    constexpr int stage = decltype(stage_c)::value;
+    copy16_at<stage * kS1TileBytes + 0 * 1024>(kpool + (uint64_t)coff[0] * 16 + kchunk[0], ring_base);
+    copy16_at<stage * kS1TileBytes + 1 * 1024>(kpool + (uint64_t)coff[1] * 16 + kchunk[1], ring_base);
+    copy16_at<stage * kS1TileBytes + 2 * 1024>(kpool + (uint64_t)coff[2] * 16 + kchunk[2], ring_base);
+    copy16_at<stage * kS1TileBytes + 3 * 1024>(kpool + (uint64_t)coff[3] * 16 + kchunk[3], ring_base);
+  };
+  // the 64 query rows of block blk (rows past R repeat row 0): wave w copies
+  // rows 16w..16w+15, copy r rows 16w + 4r + gq
+  auto issue_q = [&](int blk) __attribute__((always_inline)) {
+    const char* qsrc[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int rr = 16 * wave + 4 * r + gq;
+      int gr = blk * kS1Rows + rr;
+      if (gr >= R) gr = 0;
+      const int w = gr / g.G, gi = gr - w * g.G;
+      qsrc[r] = qunit + ((int64_t)w * g.Hq + h * g.G + gi) * kS1RowBytes + ((li ^ s1_swz(rr & 15)) * 16);
+    }
+    copy16_at<0 * 4 * kS1RowBytes>(qsrc[0], qbuf_base);
+    copy16_at<1 * 4 * kS1RowBytes>(qsrc[1], qbuf_base);
+    copy16_at<2 * 4 * kS1RowBytes>(qsrc[2], qbuf_base);
+    copy16_at<3 * 4 * kS1RowBytes>(qsrc[3], qbuf_base);
+  };
+
+  // per-lane LDS byte offsets of a tile's key operand (key li, chunk gq*4+ks)
+  int koff[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) koff[ks] = li * kS1RowBytes + (((gq * 4 + ks) ^ s1_swz(li)) * 16);
+
+  // prologue: the first block's queries, then tiles 0..D-1
+  issue_q(b0);
+  static_for<0, D>([&](auto j_c) __attribute__((always_inline)) {
+    read_offsets(decltype(j_c)::value % NT);
+    issue_k(std::integral_constant<int, decltype(j_c)::value % S>{});
+  });
+  read_offsets(D % NT);
+
+  bf16x8 qa[4][4];        // [row tile][k step]
+  bf16x8 kb[2][4];        // key operands of two tiles
+  floatx4 acc[2][4];      // logits of two tiles: [buffer][row tile], rows 4gq+q, key li
+  float m[4][4], L[4][4];
+  uint32_t es[NT][2][4];  // fp16 weight pairs: [tile][row tile pair][q], rows (2p, 2p+1)
+  float colacc[NT / 4];
+#pragma unroll
+  for (int j = 0; j < NT / 4; ++j) colacc[j] = 0.f;
+
+  auto kread = [&](int stage, int b) __attribute__((always_inline)) {
+    const char* sb = &kring[wave][stage][0];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const uint4 v = *(const uint4*)(sb + koff[ks]);
+      __builtin_memcpy(&kb[b][ks], &v, 16);
+    }
+  };
+  auto form = [&](int b) __attribute__((always_inline)) {
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      floatx4 x = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[rt][ks], kb[b][ks], x, 0, 0, 0);
+      acc[b][rt] = x;
+    }
+  };
+  // keys of tile `tile` past N: logits -inf
+  auto mask = [&](int tile, int b) __attribute__((always_inline)) {
+    if (FULL) return;
+    if ((wt0 + tile + 1) * 16 > N && (wt0 + tile) * 16 + li >= N) {
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) acc[b][rt] = floatx4{kNegInf, kNegInf, kNegInf, kNegInf};
+    }
+  };
+  auto vexp = [&](int tile, int b) __attribute__((always_inline)) {
+    float e[4][4];
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        e[rt][q] = __builtin_amdgcn_exp2f(fmaf(acc[b][rt][q], c, -m[rt][q]));
+        L[rt][q] += e[rt][q];
+      }
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) es[tile][p][q] = s1_to_agpr(s1_pack(e[2 * p][q], e[2 * p + 1][q]));
+  };
+  // row reference from the four waves' maxima mx (x = logit * c, per lane)
+  auto share_max = [&](float (&mx)[4][4]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) mx[rt][q] = dpp_max16(mx[rt][q]);
+    if (li == 0) {
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt)
+        *(float4*)&smax[wave][rt * 16 + 4 * gq] = float4{mx[rt][0], mx[rt][1], mx[rt][2], mx[rt][3]};
+    }
+    lds_barrier();
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt) {
+      float4 v = *(const float4*)&smax[0][rt * 16 + 4 * gq];
+#pragma unroll
+      for (int w = 1; w < kS1Waves; ++w) {
+        const float4 o = *(const float4*)&smax[w][rt * 16 + 4 * gq];
+        v = float4{fmaxf(v.x, o.x), fmaxf(v.y, o.y), fmaxf(v.z, o.z), fmaxf(v.w, o.w)};
+      }
+      m[rt][0] = v.x - kS1Headroom;
+      m[rt][1] = v.y - kS1Headroom;
+      m[rt][2] = v.z - kS1Headroom;
+      m[rt][3] = v.w - kS1Headroom;
+    }
+  };
+
+  // wait for tile 0's copies (the queries are older still) and publish both
+  wait_vm<4 * (D - 1)>();
+  lds_barrier();
+  kread(0, 0);
+
+  // vmcnt for tile t+1's copies at iteration t: tiles t+2..t+D-1 are newer,
+  // and the next block's queries when copied in between
+  auto wait_next = [&](auto it_c) __attribute__((always_inline)) {
+    constexpr int it = decltype(it_c)::value;
+    if constexpr (kS1QIt <= it - 1 && it + 1 <= kS1QIt + D) wait_vm<4 * (D - 2) + 4>();
+    else wait_vm<4 * (D - 2)>();
+  };
+
+  // One pass over the block's key tiles.  Iteration it: operands of tile
+  // it+1 (the next block's tile 0 at the end) into kb, logits of tile it,
+  // weights of tile it-1, copies of tile it+D into the stage tile it-1 left.
+  auto run_block = [&](bool m_given, int blk) __attribute__((always_inline)) {
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) L[rt][q] = 0.f;
+    static_for<0, NT>([&](auto it_c) __attribute__((always_inline)) {
+      constexpr int it = decltype(it_c)::value;
+      constexpr int b = it & 1;
+      wait_next(it_c);
+      kread((it + 1) % S, b ^ 1);
+      if (it < nvalid) {
+        form(b);
+        mask(it, b);
+      }
+      if (it == 1) {
+        // the shared reference, from every wave's tile 0
+        if (!m_given) {
+          float mx[4][4];
+#pragma unroll
+          for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) mx[rt][q] = nvalid > 0 ? acc[0][rt][q] * c : kNegInf;
+          share_max(mx);
+        }
+        if (nvalid > 0) vexp(0, 0);
+      } else if (it > 1 && it - 1 < nvalid) {
+        vexp(it - 1, b ^ 1);
+      }
+      issue_k(std::integral_constant<int, (it + D) % S>{});
+      read_offsets((it + D + 1) % NT);
+      if (it == kS1QIt) issue_q(min(blk + 1, nblk - 1));
+    });
+    if (NT - 1 < nvalid) vexp(NT - 1, (NT - 1) & 1);
+  };
+
+  // exact row maxima over this wave's keys, read straight from the pool
+  auto exact_max = [&]() {
+    float mx[4][4];
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) mx[rt][q] = kNegInf;
+    for (int tile = 0; tile < nvalid; ++tile) {
+      const char* src = kpool + (uint64_t)key_off[(wt0 + tile) * 16 + li] * 16 + gq * 64;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const uint4 v = *(const uint4*)(src + ks * 16);
+        __builtin_memcpy(&kb[0][ks], &v, 16);
+      }
+      form(0);
+      mask(tile, 0);
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) mx[rt][q] = fmaxf(mx[rt][q], acc[0][rt][q] * c);
+    }
+    share_max(mx);
+    // kb[0] is the next pass's tile 0 again, from its stage
+    kread(0, 0);
+  };
+
+  for (int blk = b0; blk < b1; ++blk) {
+#pragma unroll
+    for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const uint4 v = *(const uint4*)(qbuf + (rt * 16 + li) * kS1RowBytes + (((gq * 4 + ks) ^ s1_swz(li)) * 16));
+        __builtin_memcpy(&qa[rt][ks], &v, 16);
+      }
+    float ltot[4][4];
+    bool m_given = false;
+    for (int pass = 0; pass < 2; ++pass) {
+      run_block(m_given, blk);
+      // this wave's row sums, then every wave's
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) L[rt][q] = dpp_sum16(L[rt][q]);
+      if (li == 0) {
+#pragma unroll
+        for (int rt = 0; rt < 4; ++rt)
+          *(float4*)&ssum[wave][rt * 16 + 4 * gq] = float4{L[rt][0], L[rt][1], L[rt][2], L[rt][3]};
+      }
+      // the next block's queries are in LDS once the copies issued after
+      // them are at most the last 4*(D-1)
+      wait_vm<4 * (D - 1)>();
+      lds_barrier();
+      bool bad = false;
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        float4 v[kS1Waves];
+#pragma unroll
+        for (int w = 0; w < kS1Waves; ++w) v[w] = *(const float4*)&ssum[w][rt * 16 + 4 * gq];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float sum = 0.f, big = 0.f;
+#pragma unroll
+          for (int w = 0; w < kS1Waves; ++w) {
+            const float x = q == 0 ? v[w].x : q == 1 ? v[w].y : q == 2 ? v[w].z : v[w].w;
+            sum += x;
+            big = fmaxf(big, x);
+          }
+          ltot[rt][q] = sum;
+          const bool live = blk * kS1Rows + rt * 16 + 4 * gq + q < R;
+          bad |= live && !(big < kF16Max);
+        }
+      }
+      if (__builtin_amdgcn_ballot_w64(bad) == 0) break;
+      exact_max();
+      m_given = true;
+    }
+
+    // ---- weighted column sums: per tile, two fp16 MFMAs over its 64 rows.
+    // A operand of row pair p: lane (gq, li) supplies for element j the
+    // weight of row (2p + (j & 1), 4gq + (j >> 1)), the rows its own B
+    // operand element j holds; lanes li < 8 the high fp16 part, li >= 8 the
+    // low part, so output rows 0-7 sum the high parts and 8-15 the low.
+    f16x8 wa[2];
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int rt = 2 * p + (j & 1), q = j >> 1;
+        const bool live = blk * kS1Rows + rt * 16 + 4 * gq + q < R;
+        const float w = live ? kS1WScale * __builtin_amdgcn_rcpf(ltot[rt][q]) : 0.f;
+        const _Float16 hi = (_Float16)w;
+        const _Float16 lo = (_Float16)(w - (float)hi);
+        wa[p][j] = li < 8 ? hi : lo;
+      }
+    static_for<0, NT>([&](auto tile_c) __attribute__((always_inline)) {
+      constexpr int tile = decltype(tile_c)::value;
+      if (tile < nvalid) {
+        floatx4 cs = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          const uint4 ev = {es[tile][p][0], es[tile][p][1], es[tile][p][2], es[tile][p][3]};
+          cs = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[p], __builtin_bit_cast(f16x8, ev), cs, 0, 0, 0);
+        }
+        // high part (lanes 0-31) plus low part (lanes 32-63) of key li
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(cs[0]), __float_as_uint(cs[0]), false, false);
+        const float v = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+        if (gq == (tile & 3)) colacc[tile >> 2] += v;
+      }
+    });
+  }
+  wait_vm<0>();
+#pragma unroll
+  for (int j = 0; j < NT / 4; ++j) {
+    const int tile = 4 * j + gq;
+    const int key = (wt0 + tile) * 16 + li;
+    if (tile < nvalid && key < N) out[key] = colacc[j] * (1.f / kS1WScale);
+  }
+}
+
 // Row tiles per wave.  At most four (512 rows per workgroup), two for fp32
 // with 128-wide heads, whose operands take twice the registers.  Fewer when
 // a unit has few query rows (scoring by a buffer or an observation window):
@@ -621,13 +1098,27 @@ hipError_t launch_d(const ScoreArgs& a, int rt, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// Tiles per wave of the single-sweep kernel for g, 0 where the two-sweep
+// kernel runs: bf16 with d = 128 and 512 < N <= 2048 (its weights of 64
+// rows x N/4 keys fit one wave's accumulation registers).
+int single_sweep_tiles(const Geom& g) {
+  if (g.dtype != KARA_BF16 || g.d != 128 || g.N <= 512 || g.N > 2048) return 0;
+  const int ntw = ((g.N + 15) / 16 + kS1Waves - 1) / kS1Waves;
+  return ntw <= 16 ? 16 : ntw <= 24 ? 24 : 32;
+}
+
 }  // namespace
 
 ScorePlan plan_score(const Geom& g, int64_t n_units) {
   (void)n_units;
   ScorePlan sp{};
-  sp.rows_wg = kScoreWaves * 16 * row_tiles(g);
   const int64_t rows = (int64_t)g.G * g.Wq;
+  sp.single_nt = single_sweep_tiles(g);
+  if (sp.single_nt) {
+    sp.rows_wg = kS1Rows * kS1BlocksPerSplit;
+  } else {
+    sp.rows_wg = kScoreWaves * 16 * row_tiles(g);
+  }
   sp.n_splits = (int)((rows + sp.rows_wg - 1) / sp.rows_wg);
   return sp;
 }
@@ -651,7 +1142,29 @@ hipError_t launch_score(const Geom& g, const ScorePlan& sp, int n_layers, const 
   if (a.n_blocks == 0) return hipSuccess;
   const int rt = sp.rows_wg / (kScoreWaves * 16);
   hipError_t e;
-  if (g.dtype == KARA_BF16)
+  if (sp.single_nt) {
+    Score1Args a1;
+    a1.s = a;
+    a1.ntw = ((g.N + 15) / 16 + kS1Waves - 1) / kS1Waves;
+    a1.bps = kS1BlocksPerSplit;
+    const dim3 grid((unsigned)a.n_blocks), block(kS1Threads);
+    const bool full = g.N == kS1Waves * 16 * sp.single_nt;
+    switch (sp.single_nt) {
+      case 16:
+        if (full) hipLaunchKernelGGL((score1_kernel<16, true>), grid, block, 0, stream, a1);
+        else hipLaunchKernelGGL((score1_kernel<16, false>), grid, block, 0, stream, a1);
+        break;
+      case 24:
+        if (full) hipLaunchKernelGGL((score1_kernel<24, true>), grid, block, 0, stream, a1);
+        else hipLaunchKernelGGL((score1_kernel<24, false>), grid, block, 0, stream, a1);
+        break;
+      default:
+        if (full) hipLaunchKernelGGL((score1_kernel<32, true>), grid, block, 0, stream, a1);
+        else hipLaunchKernelGGL((score1_kernel<32, false>), grid, block, 0, stream, a1);
+        break;
+    }
+    e = hipGetLastError();
+  } else if (g.dtype == KARA_BF16)
     e = g.d == 128 ? launch_d<KARA_BF16, 128>(a, rt, stream) : launch_d<KARA_BF16, 64>(a, rt, stream);
   else
     e = g.d == 128 ? launch_d<KARA_F32, 128>(a, rt, stream) : launch_d<KARA_F32, 64>(a, rt, stream);
