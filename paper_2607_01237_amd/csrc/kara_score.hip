@@ -617,18 +617,12 @@ __global__ __launch_bounds__(256) void split_sum_kernel(const float* __restrict_
 // through once more with m = (exact row maximum) - 6, where no term exceeds
 // 64 and no wave sum 64 * 512.
 // ---------------------------------------------------------------------------
-constexpr int kS1Threads = 256;
-constexpr int kS1Waves = kS1Threads / 64;
-constexpr int kS1Rows = 64;                // query rows per block: 4 row tiles per wave
-constexpr int kS1Stages = 8;               // key tiles in each wave's LDS ring
-constexpr int kS1Ahead = kS1Stages - 1;    // tiles copied ahead of the one being read
 constexpr int kS1QIt = 2;                  // iteration that copies the next block's queries
 constexpr int kS1RowBytes = 256;           // one bf16 row of 128
 constexpr int kS1TileBytes = 16 * kS1RowBytes;
 constexpr float kS1Headroom = 6.f;
 constexpr float kF16Max = 65504.f;
 constexpr float kS1WScale = 2097152.f;     // 2^21: row weights 1/L, L in [64, 2^18], as fp16
-constexpr int kS1BlocksPerSplit = 8;       // row blocks per workgroup (512 rows, as the two-sweep kernel)
 
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
@@ -662,19 +656,20 @@ __device__ __forceinline__ float dpp_sum16(float v) {
   return dpp_reduce16(v, [](float x, float y) { return x + y; });
 }
 
-// Direct global->LDS copy of 16 bytes per lane to LDS address base + off
-// (base wave-uniform, off a constant): lane i's bytes land at base + off +
-// 16 i.  M0 is formed by one scalar add and restored.
+// Direct global->LDS copy of 16 bytes per lane from gbase + voff (gbase
+// wave-uniform, voff a 32-bit per-lane byte offset) to LDS address lbase +
+// OFF (lbase wave-uniform): lane i's bytes land at lbase + OFF + 16 i.  M0
+// is formed by one scalar add and restored.
 template <int OFF>
-__device__ __forceinline__ void copy16_at(const void* gp, uint32_t base) {
+__device__ __forceinline__ void copy16_at(const char* gbase, uint32_t voff, uint32_t lbase) {
   uint32_t saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
-      "s_add_u32 m0, %2, %3\n\t"
-      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_add_u32 m0, %3, %4\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
-      : "v"(gp), "s"(base), "n"(OFF)
+      : "v"(voff), "s"(gbase), "s"(lbase), "n"(OFF)
       : "memory", "scc");
 }
 
@@ -700,21 +695,48 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
-// FULL: every wave's NT tiles hold keys below N (N = 64 * NT), so no tile
-// is skipped or masked.
-template <int NT, bool FULL>
-__global__ __launch_bounds__(kS1Threads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+// Geometry of one single-sweep instance: WAVES waves of RT row tiles each,
+// every wave against all kRows rows of a block and its own share of the keys.
+// Four waves (one per SIMD, 512 registers each) hold 64 rows; eight (two per
+// SIMD, 256 registers each) hold 48, so that two waves share each SIMD's
+// issue slots: a single wave issues a vector instruction at most every ~7
+// cycles, two together every ~3.5.
+template <int WAVES, int RT>
+struct S1Cfg {
+  static constexpr int kWaves = WAVES;
+  static constexpr int kThreads = 64 * WAVES;
+  static constexpr int kRT = RT;
+  static constexpr int kRows = 16 * RT;                    // query rows per block
+  static constexpr int kStages = WAVES == 4 ? 8 : 4;       // key tiles in each wave's LDS ring
+  static constexpr int kAhead = kStages - 1;               // tiles copied ahead of the one being read
+  // one wave per SIMD: double-buffered operands and logits, so a tile's
+  // vector work overlaps the next tile's MFMAs within the wave
+  static constexpr bool kPipe = WAVES == 4;
+  static constexpr int kQCopies = kRows / 4;               // query copies of a block (4 rows each)
+  static constexpr int kQMax = (kQCopies + WAVES - 1) / WAVES;   // per wave, at most
+  static constexpr int kQMin = kQCopies / WAVES;                   // per wave, at least
+  static_assert(kQMin >= 1, "every wave copies part of the queries");
+};
+
+// FULL: every wave's NT tiles hold keys below N (N = 16 * NT * waves), so
+// no tile is skipped or masked.
+template <class CF, int NT, bool FULL>
+__global__ __launch_bounds__(CF::kThreads) __attribute__((amdgpu_waves_per_eu(CF::kWaves / 4, CF::kWaves / 4)))
 void score1_kernel(Score1Args aa) {
-  static_assert(NT % kS1Stages == 0 && NT % 4 == 0, "tiles per wave: a multiple of the ring and of 4");
-  constexpr int D = kS1Ahead;
-  constexpr int S = kS1Stages;
+  constexpr int D = CF::kAhead;
+  constexpr int S = CF::kStages;
+  constexpr int RT = CF::kRT;
+  constexpr int NW = CF::kWaves;
+  constexpr int ROWS = CF::kRows;
+  constexpr int NTH = CF::kThreads;
+  static_assert(NT % S == 0 && NT % 4 == 0, "tiles per wave: a multiple of the ring and of 4");
   const ScoreArgs& a = aa.s;
-  __shared__ __attribute__((aligned(16))) char kring[kS1Waves][S][kS1TileBytes];
-  __shared__ __attribute__((aligned(16))) char qbuf[kS1Rows * kS1RowBytes];
-  // byte offset / 16 of key j's row in the K pool; entries past N repeat key 0
-  __shared__ uint32_t key_off[kS1Waves * NT * 16];
-  __shared__ __attribute__((aligned(16))) float smax[kS1Waves][kS1Rows];
-  __shared__ __attribute__((aligned(16))) float ssum[kS1Waves][kS1Rows];
+  __shared__ __attribute__((aligned(16))) char kring[NW][S][kS1TileBytes];
+  __shared__ __attribute__((aligned(16))) char qbuf[ROWS * kS1RowBytes];
+  // byte offset of key j's row in the K pool; entries past N repeat key 0
+  __shared__ uint32_t key_off[NW * NT * 16];
+  __shared__ __attribute__((aligned(16))) float smax[NW][ROWS];
+  __shared__ __attribute__((aligned(16))) float ssum[NW][ROWS];
 
   const Geom& g = a.g;
   const int tid = threadIdx.x;
@@ -736,38 +758,39 @@ void score1_kernel(Score1Args aa) {
   const int N = g.N;
   float* out = a.n_splits == 1 ? a.scores + u * (int64_t)N : a.partials + (u * a.n_splits + split) * (int64_t)N;
   if (a.status[t] != 0) {
-    for (int j = tid; j < N; j += kS1Threads) out[j] = 0.f;
+    for (int j = tid; j < N; j += NTH) out[j] = 0.f;
     return;
   }
   const int s = a.trig[t];
   const int p0 = a.win_start[s] + wi * N;
+  // (pool and queries in SGPRs: the copies address them as base + 32-bit offset)
   const char* kpool = (const char*)a.k.p[l];
   const char* qunit = a.q + (((int64_t)l * g.n_trig + t) * g.n_win + wi) * g.Wq * g.Hq * (int64_t)kS1RowBytes;
   const int R = g.G * g.Wq;
   const float c = g.scale * kLog2e;
-  const int nblk = (R + kS1Rows - 1) / kS1Rows;
+  const int nblk = (R + ROWS - 1) / ROWS;
   const int b0 = split * aa.bps;
   const int b1 = min(nblk, b0 + aa.bps);
   const int ntw = aa.ntw;
   const int T = (N + 15) / 16;
-  const int wt0 = wave * ntw;                             // this wave's first tile
+  const int wt0 = wave * ntw;                                 // this wave's first tile
   const int nvalid = FULL ? NT : max(0, min(ntw, T - wt0));   // its tiles holding a key < N
 
   {
     const int32_t* row_pages = a.bt + (int64_t)s * g.max_blocks;
-    for (int j = tid; j < kS1Waves * NT * 16; j += kS1Threads) {
+    for (int j = tid; j < NW * NT * 16; j += NTH) {
       const int pos = p0 + (j < N ? j : 0);
       const uint64_t row = ((uint64_t)row_pages[pos / g.bs] * g.Hkv + h) * g.bs + pos % g.bs;
-      key_off[j] = (uint32_t)(row * (kS1RowBytes / 16));
+      key_off[j] = (uint32_t)(row * kS1RowBytes);
     }
   }
   lds_barrier();
 
   // ---- copies.  Copy r of a tile fills slots r*64 + lane: key row kr =
-  // 4r + gq, stored chunk li holding the row's chunk li ^ swz(kr).
-  int kchunk[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) kchunk[r] = (li ^ s1_swz(4 * r + gq)) * 16;
+  // 4r + gq, stored chunk li holding the row's chunk li ^ swz(kr) =
+  // li ^ (gq << 2) ^ r; a row's byte offset is a multiple of 256, so the
+  // source is row offset ^ chunk byte offset (one three-way XOR).
+  const uint32_t cbase = (uint32_t)((li ^ (gq << 2)) << 4);
   uint32_t coff[4];
   auto read_offsets = [&](int tile) __attribute__((always_inline)) {
 #pragma unroll
@@ -776,33 +799,33 @@ void score1_kernel(Score1Args aa) {
   const uint32_t ring_base = __builtin_amdgcn_readfirstlane(
       (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)&kring[wave][0][0]);
   const uint32_t qbuf_base = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)&qbuf[16 * wave * kS1RowBytes]);
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)&qbuf[0]);
   auto issue_k = [&](auto stage_c) __attribute__((always_inline)) {
     constexpr int stage = decltype(stage_c)::value;
-    copy16_at<stage * kS1TileBytes + 0 * 1024>(kpool + (uint64_t)coff[0] * 16 + kchunk[0], ring_base);
-    copy16_at<stage * kS1TileBytes + 1 * 1024>(kpool + (uint64_t)coff[1] * 16 + kchunk[1], ring_base);
-    copy16_at<stage * kS1TileBytes + 2 * 1024>(kpool + (uint64_t)coff[2] * 16 + kchunk[2], ring_base);
-    copy16_at<stage * kS1TileBytes + 3 * 1024>(kpool + (uint64_t)coff[3] * 16 + kchunk[3], ring_base);
+    copy16_at<stage * kS1TileBytes + 0 * 1024>(kpool, coff[0] ^ cbase ^ (0u << 4), ring_base);
+    copy16_at<stage * kS1TileBytes + 1 * 1024>(kpool, coff[1] ^ cbase ^ (1u << 4), ring_base);
+    copy16_at<stage * kS1TileBytes + 2 * 1024>(kpool, coff[2] ^ cbase ^ (2u << 4), ring_base);
+    copy16_at<stage * kS1TileBytes + 3 * 1024>(kpool, coff[3] ^ cbase ^ (3u << 4), ring_base);
   };
-  // the 64 query rows of block blk (rows past R repeat row 0): wave w copies
-  // rows 16w..16w+15, copy r rows 16w + 4r + gq
+  // the query rows of block blk (rows past R repeat row 0), 4 rows a copy:
+  // wave w issues copies w, w + NW, ...; copy cq holds rows 4cq + gq
   auto issue_q = [&](int blk) __attribute__((always_inline)) {
-    const char* qsrc[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int rr = 16 * wave + 4 * r + gq;
-      int gr = blk * kS1Rows + rr;
-      if (gr >= R) gr = 0;
-      const int w = gr / g.G, gi = gr - w * g.G;
-      qsrc[r] = qunit + ((int64_t)w * g.Hq + h * g.G + gi) * kS1RowBytes + ((li ^ s1_swz(rr & 15)) * 16);
-    }
-    copy16_at<0 * 4 * kS1RowBytes>(qsrc[0], qbuf_base);
-    copy16_at<1 * 4 * kS1RowBytes>(qsrc[1], qbuf_base);
-    copy16_at<2 * 4 * kS1RowBytes>(qsrc[2], qbuf_base);
-    copy16_at<3 * 4 * kS1RowBytes>(qsrc[3], qbuf_base);
+    static_for<0, CF::kQMax>([&](auto r_c) __attribute__((always_inline)) {
+      constexpr int r = decltype(r_c)::value;
+      const int cq = wave + r * NW;
+      if (r < CF::kQMin || cq < CF::kQCopies) {
+        const int rr = 4 * cq + gq;
+        int gr = blk * ROWS + rr;
+        if (gr >= R) gr = 0;
+        const int w = gr / g.G, gi = gr - w * g.G;
+        const uint32_t qoff = (uint32_t)((w * g.Hq + h * g.G + gi) * kS1RowBytes + ((li ^ s1_swz(rr & 15)) * 16));
+        copy16_at<0>(qunit, qoff, qbuf_base + cq * 1024);
+      }
+    });
   };
 
-  // per-lane LDS byte offsets of a tile's key operand (key li, chunk gq*4+ks)
+  // per-lane LDS byte offsets of a tile's key operand (key li, chunk
+  // gq*4 + ks; the k step must name the same chunk in every lane)
   int koff[4];
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) koff[ks] = li * kS1RowBytes + (((gq * 4 + ks) ^ s1_swz(li)) * 16);
@@ -815,11 +838,15 @@ void score1_kernel(Score1Args aa) {
   });
   read_offsets(D % NT);
 
-  bf16x8 qa[4][4];        // [row tile][k step]
-  bf16x8 kb[2][4];        // key operands of two tiles
-  floatx4 acc[2][4];      // logits of two tiles: [buffer][row tile], rows 4gq+q, key li
-  float m[4][4], L[4][4];
-  uint32_t es[NT][2][4];  // fp16 weight pairs: [tile][row tile pair][q], rows (2p, 2p+1)
+  constexpr int NB = CF::kPipe ? 2 : 1;   // operand / logit buffers
+  bf16x8 qa[RT][4];       // [row tile][k step]
+  bf16x8 kb[NB][4];       // key operands
+  floatx4 acc[NB][RT];    // logits: [buffer][row tile], rows 4gq+q, key li
+  float m[RT][4], L[RT][4];
+  // fp16 weights in pairs of the same row from tiles 2s and 2s+1:
+  // es[s][rt][q] = (row (rt, 4gq+q) at key li of tile 2s, of tile 2s+1)
+  uint32_t es[NT / 2][RT][4];
+  float ep[RT][4];        // weights of the even tile of the pair in progress
   float colacc[NT / 4];
 #pragma unroll
   for (int j = 0; j < NT / 4; ++j) colacc[j] = 0.f;
@@ -832,54 +859,80 @@ void score1_kernel(Score1Args aa) {
       __builtin_memcpy(&kb[b][ks], &v, 16);
     }
   };
+  // (k step outer: the row tiles' accumulation chains interleave)
   auto form = [&](int b) __attribute__((always_inline)) {
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt) {
-      floatx4 x = {0.f, 0.f, 0.f, 0.f};
+    for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) x = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[rt][ks], kb[b][ks], x, 0, 0, 0);
-      acc[b][rt] = x;
-    }
+      for (int rt = 0; rt < RT; ++rt)
+        acc[b][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            qa[rt][ks], kb[b][ks], ks == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : acc[b][rt], 0, 0, 0);
   };
   // keys of tile `tile` past N: logits -inf
   auto mask = [&](int tile, int b) __attribute__((always_inline)) {
     if (FULL) return;
     if ((wt0 + tile + 1) * 16 > N && (wt0 + tile) * 16 + li >= N) {
 #pragma unroll
-      for (int rt = 0; rt < 4; ++rt) acc[b][rt] = floatx4{kNegInf, kNegInf, kNegInf, kNegInf};
+      for (int rt = 0; rt < RT; ++rt) acc[b][rt] = floatx4{kNegInf, kNegInf, kNegInf, kNegInf};
+    }
+  };
+  // a finished pair: round to fp16, add both to the row sums (one packed
+  // dot product per pair) and store
+  auto finish_pair = [&](int sp, const float (&eo)[RT][4]) __attribute__((always_inline)) {
+    const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t hp = s1_pack(ep[rt][q], eo[rt][q]);
+        L[rt][q] = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, hp), ones, L[rt][q], false);
+        // one wave per SIMD keeps them in accumulation registers; with two
+        // waves (256 registers each) everything fits the ordinary ones
+        if constexpr (CF::kPipe) es[sp][rt][q] = s1_to_agpr(hp);
+        else es[sp][rt][q] = hp;
+      }
+  };
+  // weights of tile `tile` from x = logit * c - m (given as e's exponent)
+  auto weights = [&](int tile, const float (&e)[RT][4]) __attribute__((always_inline)) {
+    if (tile & 1) {
+      finish_pair(tile >> 1, e);
+    } else {
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) ep[rt][q] = e[rt][q];
+      // the pair's odd tile holds no key below N
+      if (!FULL && tile + 1 >= nvalid) {
+        const float zero[RT][4] = {};
+        finish_pair(tile >> 1, zero);
+      }
     }
   };
   auto vexp = [&](int tile, int b) __attribute__((always_inline)) {
-    float e[4][4];
+    float e[RT][4];
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt)
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        e[rt][q] = __builtin_amdgcn_exp2f(fmaf(acc[b][rt][q], c, -m[rt][q]));
-        L[rt][q] += e[rt][q];
-      }
-#pragma unroll
-    for (int p = 0; p < 2; ++p)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) es[tile][p][q] = s1_to_agpr(s1_pack(e[2 * p][q], e[2 * p + 1][q]));
+      for (int q = 0; q < 4; ++q) e[rt][q] = __builtin_amdgcn_exp2f(fmaf(acc[b][rt][q], c, -m[rt][q]));
+    weights(tile, e);
   };
-  // row reference from the four waves' maxima mx (x = logit * c, per lane)
-  auto share_max = [&](float (&mx)[4][4]) __attribute__((always_inline)) {
+  // row reference from every wave's maxima mx (x = logit * c, per lane)
+  auto share_max = [&](float (&mx)[RT][4]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt)
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int q = 0; q < 4; ++q) mx[rt][q] = dpp_max16(mx[rt][q]);
     if (li == 0) {
 #pragma unroll
-      for (int rt = 0; rt < 4; ++rt)
+      for (int rt = 0; rt < RT; ++rt)
         *(float4*)&smax[wave][rt * 16 + 4 * gq] = float4{mx[rt][0], mx[rt][1], mx[rt][2], mx[rt][3]};
     }
     lds_barrier();
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt) {
+    for (int rt = 0; rt < RT; ++rt) {
       float4 v = *(const float4*)&smax[0][rt * 16 + 4 * gq];
 #pragma unroll
-      for (int w = 1; w < kS1Waves; ++w) {
+      for (int w = 1; w < NW; ++w) {
         const float4 o = *(const float4*)&smax[w][rt * 16 + 4 * gq];
         v = float4{fmaxf(v.x, o.x), fmaxf(v.y, o.y), fmaxf(v.z, o.z), fmaxf(v.w, o.w)};
       }
@@ -899,57 +952,87 @@ void score1_kernel(Score1Args aa) {
   // and the next block's queries when copied in between
   auto wait_next = [&](auto it_c) __attribute__((always_inline)) {
     constexpr int it = decltype(it_c)::value;
-    if constexpr (kS1QIt <= it - 1 && it + 1 <= kS1QIt + D) wait_vm<4 * (D - 2) + 4>();
+    if constexpr (kS1QIt <= it - 1 && it + 1 <= kS1QIt + D) wait_vm<4 * (D - 2) + CF::kQMin>();
     else wait_vm<4 * (D - 2)>();
   };
 
-  // One pass over the block's key tiles.  Iteration it: operands of tile
-  // it+1 (the next block's tile 0 at the end) into kb, logits of tile it,
-  // weights of tile it-1, copies of tile it+D into the stage tile it-1 left.
+  // One pass over the block's key tiles.  Iteration it: logits of tile it,
+  // weights of tile it-1, operands of tile it+1 (the next block's tile 0 at
+  // the end), copies of tile it+D into the stage tile it-1 left.  With one
+  // wave per SIMD the operands are read first and the weights follow the
+  // logits' MFMAs; with two, the weights come first and single buffers do.
   auto run_block = [&](bool m_given, int blk) __attribute__((always_inline)) {
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt)
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int q = 0; q < 4; ++q) L[rt][q] = 0.f;
     static_for<0, NT>([&](auto it_c) __attribute__((always_inline)) {
       constexpr int it = decltype(it_c)::value;
-      constexpr int b = it & 1;
-      wait_next(it_c);
-      kread((it + 1) % S, b ^ 1);
-      if (it < nvalid) {
-        form(b);
-        mask(it, b);
+      constexpr int b = CF::kPipe ? (it & 1) : 0;
+      constexpr int bp = CF::kPipe ? (b ^ 1) : 0;
+      if constexpr (CF::kPipe) {
+        wait_next(it_c);
+        kread((it + 1) % S, b ^ 1);
       }
-      if (it == 1) {
+      if constexpr (it == 1) {
         // the shared reference, from every wave's tile 0
+        float x0[RT][4];
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) x0[rt][q] = nvalid > 0 ? acc[bp][rt][q] * c : kNegInf;
+        if (it < nvalid) {
+          form(b);
+          mask(it, b);
+        }
         if (!m_given) {
-          float mx[4][4];
+          float mx[RT][4];   // (share_max reduces its argument in place)
 #pragma unroll
-          for (int rt = 0; rt < 4; ++rt)
+          for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) mx[rt][q] = nvalid > 0 ? acc[0][rt][q] * c : kNegInf;
+            for (int q = 0; q < 4; ++q) mx[rt][q] = x0[rt][q];
           share_max(mx);
         }
-        if (nvalid > 0) vexp(0, 0);
-      } else if (it > 1 && it - 1 < nvalid) {
-        vexp(it - 1, b ^ 1);
+        if (nvalid > 0) {
+          float e[RT][4];
+#pragma unroll
+          for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) e[rt][q] = __builtin_amdgcn_exp2f(x0[rt][q] - m[rt][q]);
+          weights(0, e);
+        }
+      } else {
+        if constexpr (!CF::kPipe) {
+          if (it > 0 && it - 1 < nvalid) vexp(it - 1, bp);
+        }
+        if (it < nvalid) {
+          form(b);
+          mask(it, b);
+        }
+        if constexpr (CF::kPipe) {
+          if (it > 0 && it - 1 < nvalid) vexp(it - 1, bp);
+        }
+      }
+      if constexpr (!CF::kPipe) {
+        wait_next(it_c);
+        kread((it + 1) % S, 0);
       }
       issue_k(std::integral_constant<int, (it + D) % S>{});
       read_offsets((it + D + 1) % NT);
       if (it == kS1QIt) issue_q(min(blk + 1, nblk - 1));
     });
-    if (NT - 1 < nvalid) vexp(NT - 1, (NT - 1) & 1);
+    if (NT - 1 < nvalid) vexp(NT - 1, CF::kPipe ? ((NT - 1) & 1) : 0);
   };
 
   // exact row maxima over this wave's keys, read straight from the pool
   auto exact_max = [&]() {
-    float mx[4][4];
+    float mx[RT][4];
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt)
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int q = 0; q < 4; ++q) mx[rt][q] = kNegInf;
     for (int tile = 0; tile < nvalid; ++tile) {
-      const char* src = kpool + (uint64_t)key_off[(wt0 + tile) * 16 + li] * 16 + gq * 64;
+      const char* src = kpool + key_off[(wt0 + tile) * 16 + li] + gq * 64;
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const uint4 v = *(const uint4*)(src + ks * 16);
@@ -958,7 +1041,7 @@ void score1_kernel(Score1Args aa) {
       form(0);
       mask(tile, 0);
 #pragma unroll
-      for (int rt = 0; rt < 4; ++rt)
+      for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
         for (int q = 0; q < 4; ++q) mx[rt][q] = fmaxf(mx[rt][q], acc[0][rt][q] * c);
     }
@@ -969,24 +1052,24 @@ void score1_kernel(Score1Args aa) {
 
   for (int blk = b0; blk < b1; ++blk) {
 #pragma unroll
-    for (int rt = 0; rt < 4; ++rt)
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const uint4 v = *(const uint4*)(qbuf + (rt * 16 + li) * kS1RowBytes + (((gq * 4 + ks) ^ s1_swz(li)) * 16));
         __builtin_memcpy(&qa[rt][ks], &v, 16);
       }
-    float ltot[4][4];
+    float ltot[RT][4];
     bool m_given = false;
     for (int pass = 0; pass < 2; ++pass) {
       run_block(m_given, blk);
       // this wave's row sums, then every wave's
 #pragma unroll
-      for (int rt = 0; rt < 4; ++rt)
+      for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
         for (int q = 0; q < 4; ++q) L[rt][q] = dpp_sum16(L[rt][q]);
       if (li == 0) {
 #pragma unroll
-        for (int rt = 0; rt < 4; ++rt)
+        for (int rt = 0; rt < RT; ++rt)
           *(float4*)&ssum[wave][rt * 16 + 4 * gq] = float4{L[rt][0], L[rt][1], L[rt][2], L[rt][3]};
       }
       // the next block's queries are in LDS once the copies issued after
@@ -995,21 +1078,21 @@ void score1_kernel(Score1Args aa) {
       lds_barrier();
       bool bad = false;
 #pragma unroll
-      for (int rt = 0; rt < 4; ++rt) {
-        float4 v[kS1Waves];
+      for (int rt = 0; rt < RT; ++rt) {
+        float4 v[NW];
 #pragma unroll
-        for (int w = 0; w < kS1Waves; ++w) v[w] = *(const float4*)&ssum[w][rt * 16 + 4 * gq];
+        for (int w = 0; w < NW; ++w) v[w] = *(const float4*)&ssum[w][rt * 16 + 4 * gq];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           float sum = 0.f, big = 0.f;
 #pragma unroll
-          for (int w = 0; w < kS1Waves; ++w) {
+          for (int w = 0; w < NW; ++w) {
             const float x = q == 0 ? v[w].x : q == 1 ? v[w].y : q == 2 ? v[w].z : v[w].w;
             sum += x;
             big = fmaxf(big, x);
           }
           ltot[rt][q] = sum;
-          const bool live = blk * kS1Rows + rt * 16 + 4 * gq + q < R;
+          const bool live = blk * ROWS + rt * 16 + 4 * gq + q < R;
           bad |= live && !(big < kF16Max);
         }
       }
@@ -1018,43 +1101,48 @@ void score1_kernel(Score1Args aa) {
       m_given = true;
     }
 
-    // ---- weighted column sums: per tile, two fp16 MFMAs over its 64 rows.
-    // A operand of row pair p: lane (gq, li) supplies for element j the
-    // weight of row (2p + (j & 1), 4gq + (j >> 1)), the rows its own B
-    // operand element j holds; lanes li < 8 the high fp16 part, li >= 8 the
-    // low part, so output rows 0-7 sum the high parts and 8-15 the low.
-    f16x8 wa[2];
+    // ---- weighted column sums: per tile pair, RT fp16 MFMAs over the
+    // block's rows, one per row tile.  B operand (pair s, row tile rt):
+    // element j = 2q + par of lane (gq, li) holds row (rt, 4gq + q) of tile
+    // 2s + par at key li.  A operand of row tile rt: lane (gq, li) -- output
+    // row li -- supplies the weight of that row to the elements of tile
+    // parity li & 1 and 0 to the others, the high fp16 part for li < 8 and
+    // the low part for li >= 8.  Output rows 4gq'+i then hold, for key li',
+    // the high (gq' < 2) or low (gq' >= 2) sum of tile 2s + (i & 1).
+    f16x8 wa[RT];
 #pragma unroll
-    for (int p = 0; p < 2; ++p)
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int rt = 2 * p + (j & 1), q = j >> 1;
-        const bool live = blk * kS1Rows + rt * 16 + 4 * gq + q < R;
+      for (int q = 0; q < 4; ++q) {
+        const bool live = blk * ROWS + rt * 16 + 4 * gq + q < R;
         const float w = live ? kS1WScale * __builtin_amdgcn_rcpf(ltot[rt][q]) : 0.f;
         const _Float16 hi = (_Float16)w;
         const _Float16 lo = (_Float16)(w - (float)hi);
-        wa[p][j] = li < 8 ? hi : lo;
+        const _Float16 part = li < 8 ? hi : lo;
+        wa[rt][2 * q] = (li & 1) == 0 ? part : (_Float16)0.f;
+        wa[rt][2 * q + 1] = (li & 1) == 1 ? part : (_Float16)0.f;
       }
-    static_for<0, NT>([&](auto tile_c) __attribute__((always_inline)) {
-      constexpr int tile = decltype(tile_c)::value;
-      if (tile < nvalid) {
+    static_for<0, NT / 2>([&](auto s_c) __attribute__((always_inline)) {
+      constexpr int sp = decltype(s_c)::value;
+      if (2 * sp < nvalid) {
         floatx4 cs = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int p = 0; p < 2; ++p) {
-          const uint4 ev = {es[tile][p][0], es[tile][p][1], es[tile][p][2], es[tile][p][3]};
-          cs = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[p], __builtin_bit_cast(f16x8, ev), cs, 0, 0, 0);
+        for (int rt = 0; rt < RT; ++rt) {
+          const uint4 ev = {es[sp][rt][0], es[sp][rt][1], es[sp][rt][2], es[sp][rt][3]};
+          cs = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[rt], __builtin_bit_cast(f16x8, ev), cs, 0, 0, 0);
         }
-        // high part (lanes 0-31) plus low part (lanes 32-63) of key li
-        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(cs[0]), __float_as_uint(cs[0]), false, false);
+        // lanes 0-31: tile 2sp, high + low; lanes 32-63: tile 2sp+1
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(cs[0]), __float_as_uint(cs[1]), false, false);
         const float v = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
-        if (gq == (tile & 3)) colacc[tile >> 2] += v;
+        if ((gq & 1) == (sp & 1)) colacc[sp >> 1] += v;
       }
     });
   }
   wait_vm<0>();
+  // colacc[j] of lane (gq, li): pair 2j + (gq & 1), tile 2(2j + (gq & 1)) + (gq >> 1)
 #pragma unroll
   for (int j = 0; j < NT / 4; ++j) {
-    const int tile = 4 * j + gq;
+    const int tile = 2 * (2 * j + (gq & 1)) + (gq >> 1);
     const int key = (wt0 + tile) * 16 + li;
     if (tile < nvalid && key < N) out[key] = colacc[j] * (1.f / kS1WScale);
   }
@@ -1098,13 +1186,31 @@ hipError_t launch_d(const ScoreArgs& a, int rt, hipStream_t stream) {
   return hipGetLastError();
 }
 
+// The single-sweep instance the launches use, and its row blocks per split
+// (consecutive blocks of one unit share a workgroup's start-up).
+using S1Use = S1Cfg<4, 4>;
+constexpr int kS1BlocksPerSplit = 8;
+
 // Tiles per wave of the single-sweep kernel for g, 0 where the two-sweep
-// kernel runs: bf16 with d = 128 and 512 < N <= 2048 (its weights of 64
-// rows x N/4 keys fit one wave's accumulation registers).
+// kernel runs: bf16 with d = 128 and 512 < N <= 2048 (its weights of the
+// block's rows x N/waves keys fit the waves' accumulation registers).
 int single_sweep_tiles(const Geom& g) {
   if (g.dtype != KARA_BF16 || g.d != 128 || g.N <= 512 || g.N > 2048) return 0;
-  const int ntw = ((g.N + 15) / 16 + kS1Waves - 1) / kS1Waves;
-  return ntw <= 16 ? 16 : ntw <= 24 ? 24 : 32;
+  // its copies address a layer's K pool and a unit's queries by 32-bit offsets
+  if ((uint64_t)g.num_pages * g.Hkv * g.bs * kS1RowBytes > 0xffffffffull) return 0;
+  if ((uint64_t)g.Wq * g.Hq * kS1RowBytes > 0xffffffffull) return 0;
+  constexpr int NW = S1Use::kWaves, S = S1Use::kStages;
+  const int ntw = ((g.N + 15) / 16 + NW - 1) / NW;
+  // the smallest multiple of the ring (and of 4) holding ntw
+  const int step = S > 4 ? S : 4;
+  return (ntw + step - 1) / step * step;
+}
+
+template <int NT>
+void launch_s1(const Score1Args& a1, bool full, hipStream_t stream) {
+  const dim3 grid((unsigned)a1.s.n_blocks), block(S1Use::kThreads);
+  if (full) hipLaunchKernelGGL((score1_kernel<S1Use, NT, true>), grid, block, 0, stream, a1);
+  else hipLaunchKernelGGL((score1_kernel<S1Use, NT, false>), grid, block, 0, stream, a1);
 }
 
 }  // namespace
@@ -1115,7 +1221,7 @@ ScorePlan plan_score(const Geom& g, int64_t n_units) {
   const int64_t rows = (int64_t)g.G * g.Wq;
   sp.single_nt = single_sweep_tiles(g);
   if (sp.single_nt) {
-    sp.rows_wg = kS1Rows * kS1BlocksPerSplit;
+    sp.rows_wg = S1Use::kRows * kS1BlocksPerSplit;
   } else {
     sp.rows_wg = kScoreWaves * 16 * row_tiles(g);
   }
@@ -1145,23 +1251,14 @@ hipError_t launch_score(const Geom& g, const ScorePlan& sp, int n_layers, const 
   if (sp.single_nt) {
     Score1Args a1;
     a1.s = a;
-    a1.ntw = ((g.N + 15) / 16 + kS1Waves - 1) / kS1Waves;
+    a1.ntw = ((g.N + 15) / 16 + S1Use::kWaves - 1) / S1Use::kWaves;
     a1.bps = kS1BlocksPerSplit;
-    const dim3 grid((unsigned)a.n_blocks), block(kS1Threads);
-    const bool full = g.N == kS1Waves * 16 * sp.single_nt;
-    switch (sp.single_nt) {
-      case 16:
-        if (full) hipLaunchKernelGGL((score1_kernel<16, true>), grid, block, 0, stream, a1);
-        else hipLaunchKernelGGL((score1_kernel<16, false>), grid, block, 0, stream, a1);
-        break;
-      case 24:
-        if (full) hipLaunchKernelGGL((score1_kernel<24, true>), grid, block, 0, stream, a1);
-        else hipLaunchKernelGGL((score1_kernel<24, false>), grid, block, 0, stream, a1);
-        break;
-      default:
-        if (full) hipLaunchKernelGGL((score1_kernel<32, true>), grid, block, 0, stream, a1);
-        else hipLaunchKernelGGL((score1_kernel<32, false>), grid, block, 0, stream, a1);
-        break;
+    const bool full = g.N == S1Use::kWaves * 16 * sp.single_nt;
+    constexpr int S = S1Use::kStages > 4 ? S1Use::kStages : 4;
+    switch (sp.single_nt / S) {
+      case 2: launch_s1<2 * S>(a1, full, stream); break;
+      case 3: launch_s1<3 * S>(a1, full, stream); break;
+      default: launch_s1<4 * S>(a1, full, stream); break;
     }
     e = hipGetLastError();
   } else if (g.dtype == KARA_BF16)

@@ -128,8 +128,9 @@ def oracle_scores(case: Case, units=None, threads=8):
 def check_p1(gpu_scores, ora_scores):
     m = ~np.isnan(ora_scores)
     err = np.abs(gpu_scores[m].astype(np.float64) - ora_scores[m].astype(np.float64))
-    bad = err > tol(ora_scores[m].astype(np.float64))
-    assert not bad.any(), f"P1: {bad.sum()} scores out of tolerance, max err {err.max():.3e}"
+    # (written so that a NaN or infinite GPU score fails)
+    bad = ~(err <= tol(ora_scores[m].astype(np.float64)))
+    assert not bad.any(), f"P1: {bad.sum()} scores out of tolerance (or not finite), max err {np.nanmax(err):.3e}"
     rel = err / np.maximum(np.abs(ora_scores[m]), 1e-30)
     return dict(max_abs=float(err.max()) if err.size else 0.0, max_rel=float(rel.max()) if rel.size else 0.0,
                 checked=int(m.sum()))

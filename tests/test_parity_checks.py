@@ -37,6 +37,28 @@ def _gpu_from(a_gpu):
     return d, k
 
 
+def test_p1_rejects_non_finite_and_out_of_tolerance_scores():
+    rng = np.random.default_rng(3)
+    ora = rng.uniform(0.0, 4.0, size=(2, 64)).astype(np.float32)
+    ora[0, 5] = 0.0
+    kc.check_p1(ora.copy(), ora)
+    near = ora * np.float32(1 + 1.5e-3)
+    kc.check_p1(near, ora)
+    for planted in (np.nan, np.inf, -np.inf):
+        got = ora.copy()
+        got[1, 7] = planted
+        with pytest.raises(AssertionError):
+            kc.check_p1(got, ora)
+    got = ora.copy()
+    got[0, 5] = 2e-5          # past the 1e-5 absolute tolerance of a zero score
+    with pytest.raises(AssertionError):
+        kc.check_p1(got, ora)
+    got = ora.copy()
+    got[1, 9] *= np.float32(1.003)
+    with pytest.raises(AssertionError):
+        kc.check_p1(got, ora)
+
+
 def test_base_case_is_what_the_comments_say():
     d, k = _gpu_from(_base())
     assert d.tolist() == [0, 2, 4] and k.tolist() == [0, 1, 2, 4, 6]
