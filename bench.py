@@ -84,7 +84,21 @@ TRAFFIC_SOURCES = {
     "score": ["paper_2607_01237_amd/csrc/kara_score.hip"],
     "select_compact": ["paper_2607_01237_amd/csrc/kara_select.hip", "paper_2607_01237_amd/csrc/kara_pages.hip"],
 }
-TRAFFIC_KERNELS = {"score": ["score_kernel", "split_sum_kernel"], "select_compact": ["compact_kernel", "select_kernel"]}
+TRAFFIC_KERNELS = {"score": ["score1_kernel", "score_kernel", "split_sum_kernel"],
+                   "select_compact": ["compact_kernel", "select_kernel"]}
+
+
+def scoring_kernel_name(p):
+    """Which scoring kernel the library runs for these parameters (the rule
+    of its plan_score: the single-sweep kernel for bf16, d = 128 and
+    512 < N <= 2048 with pools and query blocks addressable by 32-bit
+    offsets; the two-sweep kernel otherwise)."""
+    n = p["window"] - p["buffer"]
+    pool = p["num_pages"] * p["n_kv_heads"] * p["block_size"] * p["head_dim"] * 2
+    qblk = (p.get("score_queries") or p["window"]) * p["n_q_heads"] * p["head_dim"] * 2
+    if p["dtype"] == "bf16" and p["head_dim"] == 128 and 512 < n <= 2048 and pool < 2**32 and qblk < 2**32:
+        return "score1_kernel (single-sweep window scoring, Eq. 4)"
+    return "score_kernel (two-sweep window scoring, Eq. 4)"
 CALIBRATION_KERNEL = "neg_kernel"
 
 
@@ -435,7 +449,7 @@ def run_soak(args):
             "decode_steps_per_interval": n_dec, "pages": geom.num_pages,
         },
         "roofline": {
-            "kernel": "score_kernel (window scoring, Eq. 4)",
+            "kernel": scoring_kernel_name(p),
             "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s", "frac": ach / peak, "traffic": None,
             "flop_per_launch": flops, "avg_launch_ms": float(np.mean(score_ms)),
         },
@@ -918,7 +932,7 @@ def main():
             "pages": int(geom.num_pages), "units_per_step": int(units * nw), "windows_per_sequence": nw,
         },
         "roofline": {
-            "kernel": "score_kernel (window scoring, Eq. 4)",
+            "kernel": scoring_kernel_name(p),
             "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s", "frac": ach / peak,
             "traffic": traffic["score"], "flop_per_launch": flops, "avg_launch_ms": avg["score"],
         },

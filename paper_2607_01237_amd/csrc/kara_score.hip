@@ -659,18 +659,16 @@ __device__ __forceinline__ float dpp_sum16(float v) {
 // Direct global->LDS copy of 16 bytes per lane from gbase + voff (gbase
 // wave-uniform, voff a 32-bit per-lane byte offset) to LDS address lbase +
 // OFF (lbase wave-uniform): lane i's bytes land at lbase + OFF + 16 i.  M0
-// is formed by one scalar add and restored.
+// is formed by one scalar add and left clobbered (the compiler reloads it
+// where it needs it).
 template <int OFF>
 __device__ __forceinline__ void copy16_at(const char* gbase, uint32_t voff, uint32_t lbase) {
-  uint32_t saved;
   asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_add_u32 m0, %3, %4\n\t"
-      "global_load_lds_dwordx4 %1, %2\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
+      "s_add_u32 m0, %2, %3\n\t"
+      "global_load_lds_dwordx4 %0, %1"
+      :
       : "v"(voff), "s"(gbase), "s"(lbase), "n"(OFF)
-      : "memory", "scc");
+      : "memory", "scc", "m0");
 }
 
 // a packed weight pair into an accumulation register (it is only read by MFMAs)
