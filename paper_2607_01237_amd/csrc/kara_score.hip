@@ -656,6 +656,45 @@ __device__ __forceinline__ float dpp_sum16(float v) {
   return dpp_reduce16(v, [](float x, float y) { return x + y; });
 }
 
+// The same butterflies for 16 values at once, one DPP step over all of them
+// before the next (so no step reads a value written fewer than 16
+// instructions before; the leading s_nop covers the values' last writes
+// before the block).  Written as instructions because the compiler keeps a
+// separate DPP move per step, and in IEEE mode adds a quieting max before
+// every fmaxf.
+#define S1_DPP16(OP, PAT)                                                                              \
+  asm volatile("s_nop 1\n\t"                                                                           \
+               OP " %0, %0, %0 " PAT "\n\t" OP " %1, %1, %1 " PAT "\n\t" OP " %2, %2, %2 " PAT "\n\t"  \
+               OP " %3, %3, %3 " PAT "\n\t" OP " %4, %4, %4 " PAT "\n\t" OP " %5, %5, %5 " PAT "\n\t"  \
+               OP " %6, %6, %6 " PAT "\n\t" OP " %7, %7, %7 " PAT "\n\t" OP " %8, %8, %8 " PAT "\n\t"  \
+               OP " %9, %9, %9 " PAT "\n\t" OP " %10, %10, %10 " PAT "\n\t" OP " %11, %11, %11 " PAT   \
+               "\n\t" OP " %12, %12, %12 " PAT "\n\t" OP " %13, %13, %13 " PAT "\n\t" OP " %14, %14, %14 " \
+               PAT "\n\t" OP " %15, %15, %15 " PAT                                                      \
+               : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]),     \
+                 "+v"(v[7]), "+v"(v[8]), "+v"(v[9]), "+v"(v[10]), "+v"(v[11]), "+v"(v[12]), "+v"(v[13]), \
+                 "+v"(v[14]), "+v"(v[15]))
+template <bool MAX>
+__device__ __forceinline__ void dpp_reduce16x16(float (&v)[16]) {
+  if constexpr (MAX) {
+    S1_DPP16("v_max_f32_dpp", "quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf");
+    S1_DPP16("v_max_f32_dpp", "quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf");
+    S1_DPP16("v_max_f32_dpp", "row_half_mirror row_mask:0xf bank_mask:0xf");
+    S1_DPP16("v_max_f32_dpp", "row_mirror row_mask:0xf bank_mask:0xf");
+  } else {
+    S1_DPP16("v_add_f32_dpp", "quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf");
+    S1_DPP16("v_add_f32_dpp", "quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf");
+    S1_DPP16("v_add_f32_dpp", "row_half_mirror row_mask:0xf bank_mask:0xf");
+    S1_DPP16("v_add_f32_dpp", "row_mirror row_mask:0xf bank_mask:0xf");
+  }
+}
+#undef S1_DPP16
+// max of three, with no quieting of its operands
+__device__ __forceinline__ float s1_max3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
 // Direct global->LDS copy of 16 bytes per lane from gbase + voff (gbase
 // wave-uniform, voff a 32-bit per-lane byte offset) to LDS address lbase +
 // OFF (lbase wave-uniform): lane i's bytes land at lbase + OFF + 16 i.  M0
@@ -916,10 +955,14 @@ void score1_kernel(Score1Args aa) {
   };
   // row reference from every wave's maxima mx (x = logit * c, per lane)
   auto share_max = [&](float (&mx)[RT][4]) __attribute__((always_inline)) {
+    if constexpr (RT == 4) {
+      dpp_reduce16x16<true>(reinterpret_cast<float(&)[16]>(mx));
+    } else {
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
+      for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) mx[rt][q] = dpp_max16(mx[rt][q]);
+        for (int q = 0; q < 4; ++q) mx[rt][q] = dpp_max16(mx[rt][q]);
+    }
     if (li == 0) {
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
@@ -930,9 +973,10 @@ void score1_kernel(Score1Args aa) {
     for (int rt = 0; rt < RT; ++rt) {
       float4 v = *(const float4*)&smax[0][rt * 16 + 4 * gq];
 #pragma unroll
-      for (int w = 1; w < NW; ++w) {
+      for (int w = 1; w < NW; w += 2) {
         const float4 o = *(const float4*)&smax[w][rt * 16 + 4 * gq];
-        v = float4{fmaxf(v.x, o.x), fmaxf(v.y, o.y), fmaxf(v.z, o.z), fmaxf(v.w, o.w)};
+        const float4 p = w + 1 < NW ? *(const float4*)&smax[w + 1][rt * 16 + 4 * gq] : o;
+        v = float4{s1_max3(v.x, o.x, p.x), s1_max3(v.y, o.y, p.y), s1_max3(v.z, o.z, p.z), s1_max3(v.w, o.w, p.w)};
       }
       m[rt][0] = v.x - kS1Headroom;
       m[rt][1] = v.y - kS1Headroom;
@@ -1061,10 +1105,14 @@ void score1_kernel(Score1Args aa) {
     for (int pass = 0; pass < 2; ++pass) {
       run_block(m_given, blk);
       // this wave's row sums, then every wave's
+      if constexpr (RT == 4) {
+        dpp_reduce16x16<false>(reinterpret_cast<float(&)[16]>(L));
+      } else {
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
+        for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) L[rt][q] = dpp_sum16(L[rt][q]);
+          for (int q = 0; q < 4; ++q) L[rt][q] = dpp_sum16(L[rt][q]);
+      }
       if (li == 0) {
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
@@ -1087,7 +1135,7 @@ void score1_kernel(Score1Args aa) {
           for (int w = 0; w < NW; ++w) {
             const float x = q == 0 ? v[w].x : q == 1 ? v[w].y : q == 2 ? v[w].z : v[w].w;
             sum += x;
-            big = fmaxf(big, x);
+            big = s1_max3(big, x, x);
           }
           ltot[rt][q] = sum;
           const bool live = blk * ROWS + rt * 16 + 4 * gq + q < R;
@@ -1107,18 +1155,22 @@ void score1_kernel(Score1Args aa) {
     // parity li & 1 and 0 to the others, the high fp16 part for li < 8 and
     // the low part for li >= 8.  Output rows 4gq'+i then hold, for key li',
     // the high (gq' < 2) or low (gq' >= 2) sum of tile 2s + (i & 1).
-    f16x8 wa[RT];
+    // (a lane's part of a weight goes to the low or high half of its word by
+    // a shift; lanes li < 8 take the high fp16 part, the others what it
+    // leaves)
+    const uint32_t half_shift = (uint32_t)(li & 1) * 16;
+    const bool low_part = li >= 8;
+    const bool last_block = (blk + 1) * ROWS > R;
+    uint32_t wa[RT][4];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const bool live = blk * ROWS + rt * 16 + 4 * gq + q < R;
+        const bool live = !last_block || blk * ROWS + rt * 16 + 4 * gq + q < R;
         const float w = live ? kS1WScale * __builtin_amdgcn_rcpf(ltot[rt][q]) : 0.f;
-        const _Float16 hi = (_Float16)w;
-        const _Float16 lo = (_Float16)(w - (float)hi);
-        const _Float16 part = li < 8 ? hi : lo;
-        wa[rt][2 * q] = (li & 1) == 0 ? part : (_Float16)0.f;
-        wa[rt][2 * q + 1] = (li & 1) == 1 ? part : (_Float16)0.f;
+        const float hi = (float)(_Float16)w;
+        const _Float16 part = (_Float16)(w - (low_part ? hi : 0.f));
+        wa[rt][q] = (uint32_t)__builtin_bit_cast(uint16_t, part) << half_shift;
       }
     static_for<0, NT / 2>([&](auto s_c) __attribute__((always_inline)) {
       constexpr int sp = decltype(s_c)::value;
@@ -1127,7 +1179,9 @@ void score1_kernel(Score1Args aa) {
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) {
           const uint4 ev = {es[sp][rt][0], es[sp][rt][1], es[sp][rt][2], es[sp][rt][3]};
-          cs = __builtin_amdgcn_mfma_f32_16x16x32_f16(wa[rt], __builtin_bit_cast(f16x8, ev), cs, 0, 0, 0);
+          const uint4 av = {wa[rt][0], wa[rt][1], wa[rt][2], wa[rt][3]};
+          cs = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, av), __builtin_bit_cast(f16x8, ev), cs,
+                                                      0, 0, 0);
         }
         // lanes 0-31: tile 2sp, high + low; lanes 32-63: tile 2sp+1
         const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(cs[0]), __float_as_uint(cs[1]), false, false);
