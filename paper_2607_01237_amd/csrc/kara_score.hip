@@ -656,12 +656,19 @@ __device__ __forceinline__ float dpp_sum16(float v) {
   return dpp_reduce16(v, [](float x, float y) { return x + y; });
 }
 
-// The same butterflies for 16 values at once, one DPP step over all of them
-// before the next (so no step reads a value written fewer than 16
+// The same butterflies for 8 or 16 values at once, one DPP step over all of
+// them before the next (so no step reads a value written fewer than 8
 // instructions before; the leading s_nop covers the values' last writes
 // before the block).  Written as instructions because the compiler keeps a
 // separate DPP move per step, and in IEEE mode adds a quieting max before
 // every fmaxf.
+#define S1_DPP8(OP, PAT)                                                                               \
+  asm volatile("s_nop 1\n\t"                                                                           \
+               OP " %0, %0, %0 " PAT "\n\t" OP " %1, %1, %1 " PAT "\n\t" OP " %2, %2, %2 " PAT "\n\t"  \
+               OP " %3, %3, %3 " PAT "\n\t" OP " %4, %4, %4 " PAT "\n\t" OP " %5, %5, %5 " PAT "\n\t"  \
+               OP " %6, %6, %6 " PAT "\n\t" OP " %7, %7, %7 " PAT                                        \
+               : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]),     \
+                 "+v"(v[7]))
 #define S1_DPP16(OP, PAT)                                                                              \
   asm volatile("s_nop 1\n\t"                                                                           \
                OP " %0, %0, %0 " PAT "\n\t" OP " %1, %1, %1 " PAT "\n\t" OP " %2, %2, %2 " PAT "\n\t"  \
@@ -673,21 +680,30 @@ __device__ __forceinline__ float dpp_sum16(float v) {
                : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]),     \
                  "+v"(v[7]), "+v"(v[8]), "+v"(v[9]), "+v"(v[10]), "+v"(v[11]), "+v"(v[12]), "+v"(v[13]), \
                  "+v"(v[14]), "+v"(v[15]))
-template <bool MAX>
-__device__ __forceinline__ void dpp_reduce16x16(float (&v)[16]) {
-  if constexpr (MAX) {
-    S1_DPP16("v_max_f32_dpp", "quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf");
-    S1_DPP16("v_max_f32_dpp", "quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf");
-    S1_DPP16("v_max_f32_dpp", "row_half_mirror row_mask:0xf bank_mask:0xf");
-    S1_DPP16("v_max_f32_dpp", "row_mirror row_mask:0xf bank_mask:0xf");
+#define S1_DPP_ALL(M)                                                      \
+  if constexpr (MAX) {                                                     \
+    M("v_max_f32_dpp", "quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf");  \
+    M("v_max_f32_dpp", "quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf");  \
+    M("v_max_f32_dpp", "row_half_mirror row_mask:0xf bank_mask:0xf");      \
+    M("v_max_f32_dpp", "row_mirror row_mask:0xf bank_mask:0xf");           \
+  } else {                                                                 \
+    M("v_add_f32_dpp", "quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf");  \
+    M("v_add_f32_dpp", "quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf");  \
+    M("v_add_f32_dpp", "row_half_mirror row_mask:0xf bank_mask:0xf");      \
+    M("v_add_f32_dpp", "row_mirror row_mask:0xf bank_mask:0xf");           \
+  }
+template <bool MAX, int N>
+__device__ __forceinline__ void dpp_reduce16xn(float (&v)[N]) {
+  static_assert(N == 8 || N == 16, "8 or 16 values");
+  if constexpr (N == 16) {
+    S1_DPP_ALL(S1_DPP16)
   } else {
-    S1_DPP16("v_add_f32_dpp", "quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf");
-    S1_DPP16("v_add_f32_dpp", "quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf");
-    S1_DPP16("v_add_f32_dpp", "row_half_mirror row_mask:0xf bank_mask:0xf");
-    S1_DPP16("v_add_f32_dpp", "row_mirror row_mask:0xf bank_mask:0xf");
+    S1_DPP_ALL(S1_DPP8)
   }
 }
+#undef S1_DPP_ALL
 #undef S1_DPP16
+#undef S1_DPP8
 // max of three, with no quieting of its operands
 __device__ __forceinline__ float s1_max3(float a, float b, float c) {
   float r;
@@ -695,19 +711,40 @@ __device__ __forceinline__ float s1_max3(float a, float b, float c) {
   return r;
 }
 
-// Direct global->LDS copy of 16 bytes per lane from gbase + voff (gbase
-// wave-uniform, voff a 32-bit per-lane byte offset) to LDS address lbase +
-// OFF (lbase wave-uniform): lane i's bytes land at lbase + OFF + 16 i.  M0
-// is formed by one scalar add and left clobbered (the compiler reloads it
-// where it needs it).
-template <int OFF>
-__device__ __forceinline__ void copy16_at(const char* gbase, uint32_t voff, uint32_t lbase) {
-  asm volatile(
-      "s_add_u32 m0, %2, %3\n\t"
-      "global_load_lds_dwordx4 %0, %1"
-      :
-      : "v"(voff), "s"(gbase), "s"(lbase), "n"(OFF)
-      : "memory", "scc", "m0");
+// N direct global->LDS copies of 16 bytes per lane under one M0: copy j
+// moves lane i's bytes from g[j] + voff[j] + 1024 j to LDS address lbase +
+// OFF + 1024 j + 16 i (the instruction offset moves both addresses, so the
+// callers fold its 1024 j out of the wave-uniform bases g[j]).  M0 is formed
+// by one scalar add and left clobbered.
+template <int OFF, int N>
+__device__ __forceinline__ void copy_n(const uint64_t (&g)[N], const uint32_t (&voff)[N], uint32_t lbase) {
+  static_assert(N == 1 || N == 2 || N == 4, "one, two or four copies");
+  if constexpr (N == 4)
+    asm volatile(
+        "s_add_u32 m0, %4, %5\n\t"
+        "global_load_lds_dwordx4 %0, %6\n\t"
+        "global_load_lds_dwordx4 %1, %7 offset:1024\n\t"
+        "global_load_lds_dwordx4 %2, %8 offset:2048\n\t"
+        "global_load_lds_dwordx4 %3, %9 offset:3072"
+        :
+        : "v"(voff[0]), "v"(voff[1]), "v"(voff[2]), "v"(voff[3]), "s"(lbase), "n"(OFF), "s"(g[0]), "s"(g[1]),
+          "s"(g[2]), "s"(g[3])
+        : "memory", "scc", "m0");
+  else if constexpr (N == 2)
+    asm volatile(
+        "s_add_u32 m0, %2, %3\n\t"
+        "global_load_lds_dwordx4 %0, %4\n\t"
+        "global_load_lds_dwordx4 %1, %5 offset:1024"
+        :
+        : "v"(voff[0]), "v"(voff[1]), "s"(lbase), "n"(OFF), "s"(g[0]), "s"(g[1])
+        : "memory", "scc", "m0");
+  else
+    asm volatile(
+        "s_add_u32 m0, %1, %2\n\t"
+        "global_load_lds_dwordx4 %0, %3"
+        :
+        : "v"(voff[0]), "s"(lbase), "n"(OFF), "s"(g[0])
+        : "memory", "scc", "m0");
 }
 
 // a packed weight pair into an accumulation register (it is only read by MFMAs)
@@ -732,27 +769,40 @@ __device__ __forceinline__ void static_for(F&& f) {
   }
 }
 
-// Geometry of one single-sweep instance: WAVES waves of RT row tiles each,
-// every wave against all kRows rows of a block and its own share of the keys.
-// Four waves (one per SIMD, 512 registers each) hold 64 rows; eight (two per
-// SIMD, 256 registers each) hold 48, so that two waves share each SIMD's
-// issue slots: a single wave issues a vector instruction at most every ~7
-// cycles, two together every ~3.5.
+// Geometry of one single-sweep instance: WAVES waves of RT row tiles each.
+// The keys are split in four quarters (one per SIMD) and the block's rows in
+// WAVES/4 groups; wave w takes key quarter w % 4 and row group w / 4.  Four
+// waves (one per SIMD, 512 registers each) hold 64 rows as one group; eight
+// (two per SIMD, 256 registers each) hold them as two groups of 32, so that
+// two waves share each SIMD's issue slots: a single wave issues a vector
+// instruction at most every ~7 cycles, two together every ~3.5.
 template <int WAVES, int RT>
 struct S1Cfg {
   static constexpr int kWaves = WAVES;
   static constexpr int kThreads = 64 * WAVES;
   static constexpr int kRT = RT;
-  static constexpr int kRows = 16 * RT;                    // query rows per block
-  static constexpr int kStages = WAVES == 4 ? 8 : 4;       // key tiles in each wave's LDS ring
+  static constexpr int kKQ = 4;                            // key quarters
+  static constexpr int kRG = WAVES / kKQ;                  // row groups
+  static constexpr int kWaveRows = 16 * RT;                // query rows of a wave
+  static constexpr int kRows = kWaveRows * kRG;            // query rows per block
+  // one LDS ring of key tiles per key quarter, shared by its row groups:
+  // each wave copies kCW of a tile's four 1 KB parts, and with more than one
+  // group the waves meet at a barrier before every tile's operands are read
+  static constexpr int kStages = 8;                        // key tiles in a ring
   static constexpr int kAhead = kStages - 1;               // tiles copied ahead of the one being read
-  // one wave per SIMD: double-buffered operands and logits, so a tile's
-  // vector work overlaps the next tile's MFMAs within the wave
-  static constexpr bool kPipe = WAVES == 4;
+  static constexpr int kCW = 4 / kRG;                      // copies of a tile per wave
+  // Logits are double-buffered, so a tile's vector work follows the next
+  // tile's MFMAs.  One wave per SIMD also double-buffers the key operands
+  // (read before the MFMAs) and keeps the weights in accumulation registers;
+  // with two, the operands are read between the MFMAs and the vector work,
+  // after the tile's barrier, and the weights fit the ordinary registers.
+  static constexpr bool kAgpr = WAVES == 4;
+  static constexpr int kKbBuf = WAVES == 4 ? 2 : 1;
   static constexpr int kQCopies = kRows / 4;               // query copies of a block (4 rows each)
   static constexpr int kQMax = (kQCopies + WAVES - 1) / WAVES;   // per wave, at most
   static constexpr int kQMin = kQCopies / WAVES;                   // per wave, at least
   static_assert(kQMin >= 1, "every wave copies part of the queries");
+  static_assert(WAVES % kKQ == 0 && kRG >= 1 && 4 % kRG == 0, "whole row groups, whole copies");
 };
 
 // FULL: every wave's NT tiles hold keys below N (N = 16 * NT * waves), so
@@ -766,14 +816,19 @@ void score1_kernel(Score1Args aa) {
   constexpr int NW = CF::kWaves;
   constexpr int ROWS = CF::kRows;
   constexpr int NTH = CF::kThreads;
+  constexpr int KQ = CF::kKQ;
+  constexpr int WROWS = CF::kWaveRows;
   static_assert(NT % S == 0 && NT % 4 == 0, "tiles per wave: a multiple of the ring and of 4");
   const ScoreArgs& a = aa.s;
-  __shared__ __attribute__((aligned(16))) char kring[NW][S][kS1TileBytes];
+  __shared__ __attribute__((aligned(16))) char kring[CF::kKQ][S][kS1TileBytes];
   __shared__ __attribute__((aligned(16))) char qbuf[ROWS * kS1RowBytes];
   // byte offset of key j's row in the K pool; entries past N repeat key 0
-  __shared__ uint32_t key_off[NW * NT * 16];
-  __shared__ __attribute__((aligned(16))) float smax[NW][ROWS];
-  __shared__ __attribute__((aligned(16))) float ssum[NW][ROWS];
+  __shared__ uint32_t key_off[KQ * NT * 16];
+  // per key quarter: row maxima of the first tiles, row sums
+  __shared__ __attribute__((aligned(16))) float smax[KQ][ROWS];
+  __shared__ __attribute__((aligned(16))) float ssum[KQ][ROWS];
+  // per wave: a row sum of the block reached fp16's largest value
+  __shared__ __attribute__((aligned(16))) int sbad[NW];
 
   const Geom& g = a.g;
   const int tid = threadIdx.x;
@@ -781,6 +836,10 @@ void score1_kernel(Score1Args aa) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int gq = lane >> 4;
   const int li = lane & 15;
+  const int kq = wave % KQ;              // key quarter
+  const int rg = wave / KQ;              // row group
+  const int rbase = rg * WROWS;          // first block row of this wave
+  constexpr int CW = CF::kCW;
 
   // the row splits of one unit run together on one XCD (its L2 keeps the keys)
   int64_t bid = blockIdx.x;
@@ -810,12 +869,12 @@ void score1_kernel(Score1Args aa) {
   const int b1 = min(nblk, b0 + aa.bps);
   const int ntw = aa.ntw;
   const int T = (N + 15) / 16;
-  const int wt0 = wave * ntw;                                 // this wave's first tile
+  const int wt0 = kq * ntw;                                   // this wave's first tile
   const int nvalid = FULL ? NT : max(0, min(ntw, T - wt0));   // its tiles holding a key < N
 
   {
     const int32_t* row_pages = a.bt + (int64_t)s * g.max_blocks;
-    for (int j = tid; j < NW * NT * 16; j += NTH) {
+    for (int j = tid; j < KQ * NT * 16; j += NTH) {
       const int pos = p0 + (j < N ? j : 0);
       const uint64_t row = ((uint64_t)row_pages[pos / g.bs] * g.Hkv + h) * g.bs + pos % g.bs;
       key_off[j] = (uint32_t)(row * kS1RowBytes);
@@ -828,21 +887,31 @@ void score1_kernel(Score1Args aa) {
   // li ^ (gq << 2) ^ r; a row's byte offset is a multiple of 256, so the
   // source is row offset ^ chunk byte offset (one three-way XOR).
   const uint32_t cbase = (uint32_t)((li ^ (gq << 2)) << 4);
-  uint32_t coff[4];
+  // (this wave's copies of a tile: r = rg*CW .. rg*CW + CW-1)
+  uint32_t coff[CW];
   auto read_offsets = [&](int tile) __attribute__((always_inline)) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) coff[r] = key_off[(wt0 + tile) * 16 + 4 * r + gq];
+    for (int r = 0; r < CW; ++r) coff[r] = key_off[(wt0 + tile) * 16 + 4 * (rg * CW + r) + gq];
   };
   const uint32_t ring_base = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)&kring[wave][0][0]);
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)&kring[kq][0][0]);
   const uint32_t qbuf_base = __builtin_amdgcn_readfirstlane(
       (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)&qbuf[0]);
+  // (one M0 per tile: copy j's base folds out the 1024 j its offset adds)
+  uint64_t kbase[CW];
+  uint32_t cxor[CW];
+#pragma unroll
+  for (int j = 0; j < CW; ++j) {
+    kbase[j] = (uint64_t)(uintptr_t)kpool - 1024 * j;
+    cxor[j] = cbase ^ ((uint32_t)(rg * CW + j) << 4);
+  }
+  const uint32_t kring_part = ring_base + rg * CW * 1024;
   auto issue_k = [&](auto stage_c) __attribute__((always_inline)) {
     constexpr int stage = decltype(stage_c)::value;
-    copy16_at<stage * kS1TileBytes + 0 * 1024>(kpool, coff[0] ^ cbase ^ (0u << 4), ring_base);
-    copy16_at<stage * kS1TileBytes + 1 * 1024>(kpool, coff[1] ^ cbase ^ (1u << 4), ring_base);
-    copy16_at<stage * kS1TileBytes + 2 * 1024>(kpool, coff[2] ^ cbase ^ (2u << 4), ring_base);
-    copy16_at<stage * kS1TileBytes + 3 * 1024>(kpool, coff[3] ^ cbase ^ (3u << 4), ring_base);
+    uint32_t vo[CW];
+#pragma unroll
+    for (int j = 0; j < CW; ++j) vo[j] = coff[j] ^ cxor[j];
+    copy_n<stage * kS1TileBytes>(kbase, vo, kring_part);
   };
   // the query rows of block blk (rows past R repeat row 0), 4 rows a copy:
   // wave w issues copies w, w + NW, ...; copy cq holds rows 4cq + gq
@@ -855,8 +924,9 @@ void score1_kernel(Score1Args aa) {
         int gr = blk * ROWS + rr;
         if (gr >= R) gr = 0;
         const int w = gr / g.G, gi = gr - w * g.G;
-        const uint32_t qoff = (uint32_t)((w * g.Hq + h * g.G + gi) * kS1RowBytes + ((li ^ s1_swz(rr & 15)) * 16));
-        copy16_at<0>(qunit, qoff, qbuf_base + cq * 1024);
+        const uint64_t qb[1] = {(uint64_t)(uintptr_t)qunit};
+        const uint32_t qoff[1] = {(uint32_t)((w * g.Hq + h * g.G + gi) * kS1RowBytes + ((li ^ s1_swz(rr & 15)) * 16))};
+        copy_n<0>(qb, qoff, qbuf_base + cq * 1024);
       }
     });
   };
@@ -875,10 +945,9 @@ void score1_kernel(Score1Args aa) {
   });
   read_offsets(D % NT);
 
-  constexpr int NB = CF::kPipe ? 2 : 1;   // operand / logit buffers
-  bf16x8 qa[RT][4];       // [row tile][k step]
-  bf16x8 kb[NB][4];       // key operands
-  floatx4 acc[NB][RT];    // logits: [buffer][row tile], rows 4gq+q, key li
+  bf16x8 qa[RT][4];                // [row tile][k step]
+  bf16x8 kb[CF::kKbBuf][4];        // key operands
+  floatx4 acc[2][RT];              // logits: [buffer][row tile], rows 4gq+q, key li
   float m[RT][4], L[RT][4];
   // fp16 weights in pairs of the same row from tiles 2s and 2s+1:
   // es[s][rt][q] = (row (rt, 4gq+q) at key li of tile 2s, of tile 2s+1)
@@ -889,7 +958,7 @@ void score1_kernel(Score1Args aa) {
   for (int j = 0; j < NT / 4; ++j) colacc[j] = 0.f;
 
   auto kread = [&](int stage, int b) __attribute__((always_inline)) {
-    const char* sb = &kring[wave][stage][0];
+    const char* sb = &kring[kq][stage][0];
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
       const uint4 v = *(const uint4*)(sb + koff[ks]);
@@ -897,13 +966,13 @@ void score1_kernel(Score1Args aa) {
     }
   };
   // (k step outer: the row tiles' accumulation chains interleave)
-  auto form = [&](int b) __attribute__((always_inline)) {
+  auto form = [&](int b, int kbi) __attribute__((always_inline)) {
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
         acc[b][rt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-            qa[rt][ks], kb[b][ks], ks == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : acc[b][rt], 0, 0, 0);
+            qa[rt][ks], kb[kbi][ks], ks == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : acc[b][rt], 0, 0, 0);
   };
   // keys of tile `tile` past N: logits -inf
   auto mask = [&](int tile, int b) __attribute__((always_inline)) {
@@ -925,7 +994,7 @@ void score1_kernel(Score1Args aa) {
         L[rt][q] = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, hp), ones, L[rt][q], false);
         // one wave per SIMD keeps them in accumulation registers; with two
         // waves (256 registers each) everything fits the ordinary ones
-        if constexpr (CF::kPipe) es[sp][rt][q] = s1_to_agpr(hp);
+        if constexpr (CF::kAgpr) es[sp][rt][q] = s1_to_agpr(hp);
         else es[sp][rt][q] = hp;
       }
   };
@@ -955,8 +1024,8 @@ void score1_kernel(Score1Args aa) {
   };
   // row reference from every wave's maxima mx (x = logit * c, per lane)
   auto share_max = [&](float (&mx)[RT][4]) __attribute__((always_inline)) {
-    if constexpr (RT == 4) {
-      dpp_reduce16x16<true>(reinterpret_cast<float(&)[16]>(mx));
+    if constexpr (RT == 4 || RT == 2) {
+      dpp_reduce16xn<true, RT * 4>(reinterpret_cast<float(&)[RT * 4]>(mx));
     } else {
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
@@ -966,16 +1035,16 @@ void score1_kernel(Score1Args aa) {
     if (li == 0) {
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
-        *(float4*)&smax[wave][rt * 16 + 4 * gq] = float4{mx[rt][0], mx[rt][1], mx[rt][2], mx[rt][3]};
+        *(float4*)&smax[kq][rbase + rt * 16 + 4 * gq] = float4{mx[rt][0], mx[rt][1], mx[rt][2], mx[rt][3]};
     }
     lds_barrier();
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
-      float4 v = *(const float4*)&smax[0][rt * 16 + 4 * gq];
+      float4 v = *(const float4*)&smax[0][rbase + rt * 16 + 4 * gq];
 #pragma unroll
-      for (int w = 1; w < NW; w += 2) {
-        const float4 o = *(const float4*)&smax[w][rt * 16 + 4 * gq];
-        const float4 p = w + 1 < NW ? *(const float4*)&smax[w + 1][rt * 16 + 4 * gq] : o;
+      for (int w = 1; w < KQ; w += 2) {
+        const float4 o = *(const float4*)&smax[w][rbase + rt * 16 + 4 * gq];
+        const float4 p = w + 1 < KQ ? *(const float4*)&smax[w + 1][rbase + rt * 16 + 4 * gq] : o;
         v = float4{s1_max3(v.x, o.x, p.x), s1_max3(v.y, o.y, p.y), s1_max3(v.z, o.z, p.z), s1_max3(v.w, o.w, p.w)};
       }
       m[rt][0] = v.x - kS1Headroom;
@@ -986,7 +1055,7 @@ void score1_kernel(Score1Args aa) {
   };
 
   // wait for tile 0's copies (the queries are older still) and publish both
-  wait_vm<4 * (D - 1)>();
+  wait_vm<CW * (D - 1)>();
   lds_barrier();
   kread(0, 0);
 
@@ -994,15 +1063,18 @@ void score1_kernel(Score1Args aa) {
   // and the next block's queries when copied in between
   auto wait_next = [&](auto it_c) __attribute__((always_inline)) {
     constexpr int it = decltype(it_c)::value;
-    if constexpr (kS1QIt <= it - 1 && it + 1 <= kS1QIt + D) wait_vm<4 * (D - 2) + CF::kQMin>();
-    else wait_vm<4 * (D - 2)>();
+    if constexpr (kS1QIt <= it - 1 && it + 1 <= kS1QIt + D) wait_vm<CW * (D - 2) + CF::kQMin>();
+    else wait_vm<CW * (D - 2)>();
+    // the other row groups' parts of the tile
+    if constexpr (CF::kRG > 1) lds_barrier();
   };
 
   // One pass over the block's key tiles.  Iteration it: logits of tile it,
   // weights of tile it-1, operands of tile it+1 (the next block's tile 0 at
   // the end), copies of tile it+D into the stage tile it-1 left.  With one
-  // wave per SIMD the operands are read first and the weights follow the
-  // logits' MFMAs; with two, the weights come first and single buffers do.
+  // wave per SIMD the operands are read first, into the other buffer; with
+  // two, after the logits' MFMAs are issued (and the tile's barrier), so the
+  // weights' vector work overlaps both the MFMAs and the reads.
   auto run_block = [&](bool m_given, int blk) __attribute__((always_inline)) {
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
@@ -1010,11 +1082,20 @@ void score1_kernel(Score1Args aa) {
       for (int q = 0; q < 4; ++q) L[rt][q] = 0.f;
     static_for<0, NT>([&](auto it_c) __attribute__((always_inline)) {
       constexpr int it = decltype(it_c)::value;
-      constexpr int b = CF::kPipe ? (it & 1) : 0;
-      constexpr int bp = CF::kPipe ? (b ^ 1) : 0;
-      if constexpr (CF::kPipe) {
+      constexpr int b = it & 1;                             // logits of tile it
+      constexpr int bp = b ^ 1;                             // of tile it-1
+      constexpr int kbi = CF::kKbBuf == 2 ? (it & 1) : 0;   // operands of tile it
+      if constexpr (CF::kKbBuf == 2) {
         wait_next(it_c);
-        kread((it + 1) % S, b ^ 1);
+        kread((it + 1) % S, kbi ^ 1);
+      }
+      if (it < nvalid) {
+        form(b, kbi);
+        mask(it, b);
+      }
+      if constexpr (CF::kKbBuf == 1) {
+        wait_next(it_c);
+        kread((it + 1) % S, 0);
       }
       if constexpr (it == 1) {
         // the shared reference, from every wave's tile 0
@@ -1023,10 +1104,6 @@ void score1_kernel(Score1Args aa) {
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
           for (int q = 0; q < 4; ++q) x0[rt][q] = nvalid > 0 ? acc[bp][rt][q] * c : kNegInf;
-        if (it < nvalid) {
-          form(b);
-          mask(it, b);
-        }
         if (!m_given) {
           float mx[RT][4];   // (share_max reduces its argument in place)
 #pragma unroll
@@ -1043,27 +1120,14 @@ void score1_kernel(Score1Args aa) {
             for (int q = 0; q < 4; ++q) e[rt][q] = __builtin_amdgcn_exp2f(x0[rt][q] - m[rt][q]);
           weights(0, e);
         }
-      } else {
-        if constexpr (!CF::kPipe) {
-          if (it > 0 && it - 1 < nvalid) vexp(it - 1, bp);
-        }
-        if (it < nvalid) {
-          form(b);
-          mask(it, b);
-        }
-        if constexpr (CF::kPipe) {
-          if (it > 0 && it - 1 < nvalid) vexp(it - 1, bp);
-        }
-      }
-      if constexpr (!CF::kPipe) {
-        wait_next(it_c);
-        kread((it + 1) % S, 0);
+      } else if constexpr (it > 1) {
+        if (it - 1 < nvalid) vexp(it - 1, bp);
       }
       issue_k(std::integral_constant<int, (it + D) % S>{});
       read_offsets((it + D + 1) % NT);
       if (it == kS1QIt) issue_q(min(blk + 1, nblk - 1));
     });
-    if (NT - 1 < nvalid) vexp(NT - 1, CF::kPipe ? ((NT - 1) & 1) : 0);
+    if (NT - 1 < nvalid) vexp(NT - 1, (NT - 1) & 1);
   };
 
   // exact row maxima over this wave's keys, read straight from the pool
@@ -1080,7 +1144,7 @@ void score1_kernel(Score1Args aa) {
         const uint4 v = *(const uint4*)(src + ks * 16);
         __builtin_memcpy(&kb[0][ks], &v, 16);
       }
-      form(0);
+      form(0, 0);
       mask(tile, 0);
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
@@ -1097,7 +1161,8 @@ void score1_kernel(Score1Args aa) {
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
-        const uint4 v = *(const uint4*)(qbuf + (rt * 16 + li) * kS1RowBytes + (((gq * 4 + ks) ^ s1_swz(li)) * 16));
+        const uint4 v =
+            *(const uint4*)(qbuf + (rbase + rt * 16 + li) * kS1RowBytes + (((gq * 4 + ks) ^ s1_swz(li)) * 16));
         __builtin_memcpy(&qa[rt][ks], &v, 16);
       }
     float ltot[RT][4];
@@ -1105,8 +1170,8 @@ void score1_kernel(Score1Args aa) {
     for (int pass = 0; pass < 2; ++pass) {
       run_block(m_given, blk);
       // this wave's row sums, then every wave's
-      if constexpr (RT == 4) {
-        dpp_reduce16x16<false>(reinterpret_cast<float(&)[16]>(L));
+      if constexpr (RT == 4 || RT == 2) {
+        dpp_reduce16xn<false, RT * 4>(reinterpret_cast<float(&)[RT * 4]>(L));
       } else {
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
@@ -1116,33 +1181,49 @@ void score1_kernel(Score1Args aa) {
       if (li == 0) {
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
-          *(float4*)&ssum[wave][rt * 16 + 4 * gq] = float4{L[rt][0], L[rt][1], L[rt][2], L[rt][3]};
+          *(float4*)&ssum[kq][rbase + rt * 16 + 4 * gq] = float4{L[rt][0], L[rt][1], L[rt][2], L[rt][3]};
+      }
+      // (rows past R repeat row 0, so they overflow only where row 0 did)
+      {
+        float big = L[0][0];
+        static_for<1, RT * 4 / 2 + 1>([&](auto i_c) __attribute__((always_inline)) {
+          constexpr int i = decltype(i_c)::value;
+          constexpr int j = 2 * i - 1, k = 2 * i;
+          big = s1_max3(big, L[j / 4][j % 4], L[k < RT * 4 ? k / 4 : 0][k < RT * 4 ? k % 4 : 0]);
+        });
+        const bool wbad = __builtin_amdgcn_ballot_w64(!(big < kF16Max)) != 0;
+        if (lane == 0) sbad[wave] = wbad;
       }
       // the next block's queries are in LDS once the copies issued after
       // them are at most the last 4*(D-1)
-      wait_vm<4 * (D - 1)>();
+      wait_vm<CW * (D - 1)>();
       lds_barrier();
-      bool bad = false;
+      int anybad = 0;
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        float4 v[NW];
-#pragma unroll
-        for (int w = 0; w < NW; ++w) v[w] = *(const float4*)&ssum[w][rt * 16 + 4 * gq];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          float sum = 0.f, big = 0.f;
-#pragma unroll
-          for (int w = 0; w < NW; ++w) {
-            const float x = q == 0 ? v[w].x : q == 1 ? v[w].y : q == 2 ? v[w].z : v[w].w;
-            sum += x;
-            big = s1_max3(big, x, x);
-          }
-          ltot[rt][q] = sum;
-          const bool live = blk * ROWS + rt * 16 + 4 * gq + q < R;
-          bad |= live && !(big < kF16Max);
-        }
+      for (int w = 0; w < NW; w += 4) {
+        const int4 f = *(const int4*)&sbad[w];
+        anybad |= f.x | f.y | f.z | f.w;
       }
-      if (__builtin_amdgcn_ballot_w64(bad) == 0) break;
+      if (__builtin_amdgcn_readfirstlane(anybad) == 0) {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+          float4 v[KQ];
+#pragma unroll
+          for (int w = 0; w < KQ; ++w) v[w] = *(const float4*)&ssum[w][rbase + rt * 16 + 4 * gq];
+          ltot[rt][0] = v[0].x;
+          ltot[rt][1] = v[0].y;
+          ltot[rt][2] = v[0].z;
+          ltot[rt][3] = v[0].w;
+#pragma unroll
+          for (int w = 1; w < KQ; ++w) {
+            ltot[rt][0] += v[w].x;
+            ltot[rt][1] += v[w].y;
+            ltot[rt][2] += v[w].z;
+            ltot[rt][3] += v[w].w;
+          }
+        }
+        break;
+      }
       exact_max();
       m_given = true;
     }
@@ -1166,7 +1247,7 @@ void score1_kernel(Score1Args aa) {
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const bool live = !last_block || blk * ROWS + rt * 16 + 4 * gq + q < R;
+        const bool live = !last_block || blk * ROWS + rbase + rt * 16 + 4 * gq + q < R;
         const float w = live ? kS1WScale * __builtin_amdgcn_rcpf(ltot[rt][q]) : 0.f;
         const float hi = (float)(_Float16)w;
         const _Float16 part = (_Float16)(w - (low_part ? hi : 0.f));
@@ -1191,6 +1272,23 @@ void score1_kernel(Score1Args aa) {
     });
   }
   wait_vm<0>();
+  if constexpr (CF::kRG > 1) {
+    // the row groups' column sums of one key quarter, added through its
+    // ring once every wave's copies have landed
+    static_assert((CF::kRG - 1) * NT / 4 * 64 * 4 <= S * kS1TileBytes, "column sums fit a ring");
+    lds_barrier();
+    float* part = (float*)&kring[kq][0][0];
+    if (rg != 0) {
+#pragma unroll
+      for (int j = 0; j < NT / 4; ++j) part[((rg - 1) * (NT / 4) + j) * 64 + lane] = colacc[j];
+    }
+    lds_barrier();
+    if (rg != 0) return;
+#pragma unroll
+    for (int r = 1; r < CF::kRG; ++r)
+#pragma unroll
+      for (int j = 0; j < NT / 4; ++j) colacc[j] += part[((r - 1) * (NT / 4) + j) * 64 + lane];
+  }
   // colacc[j] of lane (gq, li): pair 2j + (gq & 1), tile 2(2j + (gq & 1)) + (gq >> 1)
 #pragma unroll
   for (int j = 0; j < NT / 4; ++j) {
@@ -1251,11 +1349,11 @@ int single_sweep_tiles(const Geom& g) {
   // its copies address a layer's K pool and a unit's queries by 32-bit offsets
   if ((uint64_t)g.num_pages * g.Hkv * g.bs * kS1RowBytes > 0xffffffffull) return 0;
   if ((uint64_t)g.Wq * g.Hq * kS1RowBytes > 0xffffffffull) return 0;
-  constexpr int NW = S1Use::kWaves, S = S1Use::kStages;
-  const int ntw = ((g.N + 15) / 16 + NW - 1) / NW;
-  // the smallest multiple of the ring (and of 4) holding ntw
-  const int step = S > 4 ? S : 4;
-  return (ntw + step - 1) / step * step;
+  constexpr int KQ = S1Use::kKQ;
+  const int ntw = ((g.N + 15) / 16 + KQ - 1) / KQ;
+  // the smallest multiple of 8 (of the ring, and of 4) holding ntw
+  static_assert(8 % S1Use::kStages == 0, "instances come in steps of 8 tiles");
+  return (ntw + 7) / 8 * 8;
 }
 
 template <int NT>
@@ -1303,14 +1401,13 @@ hipError_t launch_score(const Geom& g, const ScorePlan& sp, int n_layers, const 
   if (sp.single_nt) {
     Score1Args a1;
     a1.s = a;
-    a1.ntw = ((g.N + 15) / 16 + S1Use::kWaves - 1) / S1Use::kWaves;
+    a1.ntw = ((g.N + 15) / 16 + S1Use::kKQ - 1) / S1Use::kKQ;
     a1.bps = kS1BlocksPerSplit;
-    const bool full = g.N == S1Use::kWaves * 16 * sp.single_nt;
-    constexpr int S = S1Use::kStages > 4 ? S1Use::kStages : 4;
-    switch (sp.single_nt / S) {
-      case 2: launch_s1<2 * S>(a1, full, stream); break;
-      case 3: launch_s1<3 * S>(a1, full, stream); break;
-      default: launch_s1<4 * S>(a1, full, stream); break;
+    const bool full = g.N == S1Use::kKQ * 16 * sp.single_nt;
+    switch (sp.single_nt / 8) {
+      case 2: launch_s1<16>(a1, full, stream); break;
+      case 3: launch_s1<24>(a1, full, stream); break;
+      default: launch_s1<32>(a1, full, stream); break;
     }
     e = hipGetLastError();
   } else if (g.dtype == KARA_BF16)
