@@ -618,6 +618,7 @@ __global__ __launch_bounds__(256) void split_sum_kernel(const float* __restrict_
 // 64 and no wave sum 64 * 512.
 // ---------------------------------------------------------------------------
 constexpr int kS1QIt = 2;                  // iteration that copies the next block's queries
+constexpr int kS1BlocksPerSplit = 8;       // row blocks per workgroup (consecutive blocks of one unit)
 constexpr int kS1RowBytes = 256;           // one bf16 row of 128
 constexpr int kS1TileBytes = 16 * kS1RowBytes;
 constexpr float kS1Headroom = 6.f;
@@ -631,7 +632,6 @@ typedef float float2v __attribute__((ext_vector_type(2)));
 struct Score1Args {
   ScoreArgs s;
   int ntw;          // key tiles per wave
-  int bps;          // row blocks per split
 };
 
 // the 16-byte chunk swizzle of a 256-byte row in LDS (conflict-free for the
@@ -829,6 +829,9 @@ void score1_kernel(Score1Args aa) {
   __shared__ __attribute__((aligned(16))) float ssum[KQ][ROWS];
   // per wave: a row sum of the block reached fp16's largest value
   __shared__ __attribute__((aligned(16))) int sbad[NW];
+  // byte offset of each of the split's query rows in the unit's queries
+  // (rows past R repeat row 0)
+  __shared__ uint32_t qrow_off[kS1BlocksPerSplit * ROWS];
 
   const Geom& g = a.g;
   const int tid = threadIdx.x;
@@ -865,8 +868,8 @@ void score1_kernel(Score1Args aa) {
   const int R = g.G * g.Wq;
   const float c = g.scale * kLog2e;
   const int nblk = (R + ROWS - 1) / ROWS;
-  const int b0 = split * aa.bps;
-  const int b1 = min(nblk, b0 + aa.bps);
+  const int b0 = split * kS1BlocksPerSplit;
+  const int b1 = min(nblk, b0 + kS1BlocksPerSplit);
   const int ntw = aa.ntw;
   const int T = (N + 15) / 16;
   const int wt0 = kq * ntw;                                   // this wave's first tile
@@ -878,6 +881,12 @@ void score1_kernel(Score1Args aa) {
       const int pos = p0 + (j < N ? j : 0);
       const uint64_t row = ((uint64_t)row_pages[pos / g.bs] * g.Hkv + h) * g.bs + pos % g.bs;
       key_off[j] = (uint32_t)(row * kS1RowBytes);
+    }
+    for (int j = tid; j < kS1BlocksPerSplit * ROWS; j += NTH) {
+      int gr = b0 * ROWS + j;
+      if (gr >= R) gr = 0;
+      const int w = gr / g.G, gi = gr - w * g.G;
+      qrow_off[j] = (uint32_t)((w * g.Hq + h * g.G + gi) * kS1RowBytes);
     }
   }
   lds_barrier();
@@ -921,11 +930,8 @@ void score1_kernel(Score1Args aa) {
       const int cq = wave + r * NW;
       if (r < CF::kQMin || cq < CF::kQCopies) {
         const int rr = 4 * cq + gq;
-        int gr = blk * ROWS + rr;
-        if (gr >= R) gr = 0;
-        const int w = gr / g.G, gi = gr - w * g.G;
         const uint64_t qb[1] = {(uint64_t)(uintptr_t)qunit};
-        const uint32_t qoff[1] = {(uint32_t)((w * g.Hq + h * g.G + gi) * kS1RowBytes + ((li ^ s1_swz(rr & 15)) * 16))};
+        const uint32_t qoff[1] = {qrow_off[(blk - b0) * ROWS + rr] + (uint32_t)((li ^ s1_swz(rr & 15)) * 16)};
         copy_n<0>(qb, qoff, qbuf_base + cq * 1024);
       }
     });
@@ -1125,7 +1131,8 @@ void score1_kernel(Score1Args aa) {
       }
       issue_k(std::integral_constant<int, (it + D) % S>{});
       read_offsets((it + D + 1) % NT);
-      if (it == kS1QIt) issue_q(min(blk + 1, nblk - 1));
+      // (the split's last block copies its own rows again, unused)
+      if (it == kS1QIt) issue_q(min(blk + 1, b1 - 1));
     });
     if (NT - 1 < nvalid) vexp(NT - 1, (NT - 1) & 1);
   };
@@ -1242,34 +1249,58 @@ void score1_kernel(Score1Args aa) {
     const uint32_t half_shift = (uint32_t)(li & 1) * 16;
     const bool low_part = li >= 8;
     const bool last_block = (blk + 1) * ROWS > R;
-    uint32_t wa[RT][4];
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
+    auto weights_of = [&](int rt, uint32_t (&wa)[4]) __attribute__((always_inline)) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const bool live = !last_block || blk * ROWS + rbase + rt * 16 + 4 * gq + q < R;
         const float w = live ? kS1WScale * __builtin_amdgcn_rcpf(ltot[rt][q]) : 0.f;
         const float hi = (float)(_Float16)w;
         const _Float16 part = (_Float16)(w - (low_part ? hi : 0.f));
-        wa[rt][q] = (uint32_t)__builtin_bit_cast(uint16_t, part) << half_shift;
+        wa[q] = (uint32_t)__builtin_bit_cast(uint16_t, part) << half_shift;
       }
-    static_for<0, NT / 2>([&](auto s_c) __attribute__((always_inline)) {
+    };
+    auto mfma_w = [&](const uint32_t (&wa)[4], int sp, int rt, floatx4 cin) __attribute__((always_inline)) {
+      const uint4 av = {wa[0], wa[1], wa[2], wa[3]};
+      const uint4 ev = {es[sp][rt][0], es[sp][rt][1], es[sp][rt][2], es[sp][rt][3]};
+      return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, av), __builtin_bit_cast(f16x8, ev), cin,
+                                                    0, 0, 0);
+    };
+    auto add_pair = [&](auto s_c, const floatx4& cs) __attribute__((always_inline)) {
       constexpr int sp = decltype(s_c)::value;
-      if (2 * sp < nvalid) {
-        floatx4 cs = {0.f, 0.f, 0.f, 0.f};
+      // lanes 0-31: tile 2sp, high + low; lanes 32-63: tile 2sp+1
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(cs[0]), __float_as_uint(cs[1]), false, false);
+      const float v = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+      if ((gq & 1) == (sp & 1)) colacc[sp >> 1] += v;
+    };
+    if constexpr (FULL) {
+      // row tile by row tile: its weights, then its MFMA for every pair (one
+      // accumulator per pair), so a tile's weight arithmetic overlaps the
+      // previous tile's MFMAs
+      floatx4 cs[NT / 2];
+      static_for<0, RT>([&](auto rt_c) __attribute__((always_inline)) {
+        constexpr int rt = decltype(rt_c)::value;
+        uint32_t wa[4];
+        weights_of(rt, wa);
+        static_for<0, NT / 2>([&](auto s_c) __attribute__((always_inline)) {
+          constexpr int sp = decltype(s_c)::value;
+          cs[sp] = mfma_w(wa, sp, rt, rt == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : cs[sp]);
+        });
+      });
+      static_for<0, NT / 2>([&](auto s_c) __attribute__((always_inline)) { add_pair(s_c, cs[decltype(s_c)::value]); });
+    } else {
+      uint32_t wa[RT][4];
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt) {
-          const uint4 ev = {es[sp][rt][0], es[sp][rt][1], es[sp][rt][2], es[sp][rt][3]};
-          const uint4 av = {wa[rt][0], wa[rt][1], wa[rt][2], wa[rt][3]};
-          cs = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, av), __builtin_bit_cast(f16x8, ev), cs,
-                                                      0, 0, 0);
+      for (int rt = 0; rt < RT; ++rt) weights_of(rt, wa[rt]);
+      static_for<0, NT / 2>([&](auto s_c) __attribute__((always_inline)) {
+        constexpr int sp = decltype(s_c)::value;
+        if (2 * sp < nvalid) {
+          floatx4 cs = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int rt = 0; rt < RT; ++rt) cs = mfma_w(wa[rt], sp, rt, cs);
+          add_pair(s_c, cs);
         }
-        // lanes 0-31: tile 2sp, high + low; lanes 32-63: tile 2sp+1
-        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(cs[0]), __float_as_uint(cs[1]), false, false);
-        const float v = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
-        if ((gq & 1) == (sp & 1)) colacc[sp >> 1] += v;
-      }
-    });
+      });
+    }
   }
   wait_vm<0>();
   if constexpr (CF::kRG > 1) {
@@ -1336,10 +1367,8 @@ hipError_t launch_d(const ScoreArgs& a, int rt, hipStream_t stream) {
   return hipGetLastError();
 }
 
-// The single-sweep instance the launches use, and its row blocks per split
-// (consecutive blocks of one unit share a workgroup's start-up).
+// The single-sweep instance the launches use.
 using S1Use = S1Cfg<4, 4>;
-constexpr int kS1BlocksPerSplit = 8;
 
 // Tiles per wave of the single-sweep kernel for g, 0 where the two-sweep
 // kernel runs: bf16 with d = 128 and 512 < N <= 2048 (its weights of the
@@ -1402,7 +1431,6 @@ hipError_t launch_score(const Geom& g, const ScorePlan& sp, int n_layers, const 
     Score1Args a1;
     a1.s = a;
     a1.ntw = ((g.N + 15) / 16 + S1Use::kKQ - 1) / S1Use::kKQ;
-    a1.bps = kS1BlocksPerSplit;
     const bool full = g.N == S1Use::kKQ * 16 * sp.single_nt;
     switch (sp.single_nt / 8) {
       case 2: launch_s1<16>(a1, full, stream); break;
