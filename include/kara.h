@@ -308,9 +308,9 @@ kara_status_t kara_compress_prefill(const kara_params_t* p, int32_t n_trig, cons
  *
  * Limit: the workspace kara_workspace_size() reports for (p, n_trig,
  * n_layers) must fit in KARA_NOALLOC_SCRATCH_BYTES, else the call returns
- * KARA_ERR_SCRATCH_LIMIT and enqueues nothing.  64 MiB holds about 1,700
+ * KARA_ERR_SCRATCH_LIMIT and enqueues nothing.  64 MiB holds about 3,000
  * units of a 32/8-head, W = 1024 model with scores and index sets left to
- * the library (38.4 KB each): 30 sequences x 7 layers, or one layer of 200
+ * the library (22 KB each): 53 sequences x 7 layers, or one layer of 380
  * sequences.  The array's device address is resolved once per
  * device, on the first call with that device current.
  *

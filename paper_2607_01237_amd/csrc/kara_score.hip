@@ -618,7 +618,7 @@ __global__ __launch_bounds__(256) void split_sum_kernel(const float* __restrict_
 // 64 and no wave sum 64 * 512.
 // ---------------------------------------------------------------------------
 constexpr int kS1QIt = 2;                  // iteration that copies the next block's queries
-constexpr int kS1BlocksPerSplit = 8;       // row blocks per workgroup (consecutive blocks of one unit)
+constexpr int kS1BlocksPerSplit = 16;      // row blocks per workgroup (consecutive blocks of one unit)
 constexpr int kS1RowBytes = 256;           // one bf16 row of 128
 constexpr int kS1TileBytes = 16 * kS1RowBytes;
 constexpr float kS1Headroom = 6.f;

@@ -103,7 +103,7 @@ def test_noalloc_refuses_past_its_scratch():
     from paper_2607_01237_amd import kara
     _need_gpu()
     dev = torch.device("cuda:0")
-    cfg = ki.workload("batch8", n_seqs=8, n_layers=40, window=1024, budget=205)
+    cfg = ki.workload("batch8", n_seqs=16, n_layers=40, window=1024, budget=205)
     geom = ki.make_geometry(cfg)
     p = geom.params()
     params = kara.make_params(p, geom.block_table.shape[0])
