@@ -1028,7 +1028,8 @@ void score1_kernel(Score1Args aa) {
       for (int q = 0; q < 4; ++q) e[rt][q] = __builtin_amdgcn_exp2f(fmaf(acc[b][rt][q], c, -m[rt][q]));
     weights(tile, e);
   };
-  // row reference from every wave's maxima mx (x = logit * c, per lane)
+  // row reference from every wave's maxima mx of the raw logits, per lane
+  // (c > 0, so the maximum of x = logit * c is c times theirs)
   auto share_max = [&](float (&mx)[RT][4]) __attribute__((always_inline)) {
     if constexpr (RT == 4 || RT == 2) {
       dpp_reduce16xn<true, RT * 4>(reinterpret_cast<float(&)[RT * 4]>(mx));
@@ -1053,10 +1054,10 @@ void score1_kernel(Score1Args aa) {
         const float4 p = w + 1 < KQ ? *(const float4*)&smax[w + 1][rbase + rt * 16 + 4 * gq] : o;
         v = float4{s1_max3(v.x, o.x, p.x), s1_max3(v.y, o.y, p.y), s1_max3(v.z, o.z, p.z), s1_max3(v.w, o.w, p.w)};
       }
-      m[rt][0] = v.x - kS1Headroom;
-      m[rt][1] = v.y - kS1Headroom;
-      m[rt][2] = v.z - kS1Headroom;
-      m[rt][3] = v.w - kS1Headroom;
+      m[rt][0] = fmaf(v.x, c, -kS1Headroom);
+      m[rt][1] = fmaf(v.y, c, -kS1Headroom);
+      m[rt][2] = fmaf(v.z, c, -kS1Headroom);
+      m[rt][3] = fmaf(v.w, c, -kS1Headroom);
     }
   };
 
@@ -1105,27 +1106,15 @@ void score1_kernel(Score1Args aa) {
       }
       if constexpr (it == 1) {
         // the shared reference, from every wave's tile 0
-        float x0[RT][4];
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-          for (int q = 0; q < 4; ++q) x0[rt][q] = nvalid > 0 ? acc[bp][rt][q] * c : kNegInf;
         if (!m_given) {
           float mx[RT][4];   // (share_max reduces its argument in place)
 #pragma unroll
           for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-            for (int q = 0; q < 4; ++q) mx[rt][q] = x0[rt][q];
+            for (int q = 0; q < 4; ++q) mx[rt][q] = nvalid > 0 ? acc[bp][rt][q] : kNegInf;
           share_max(mx);
         }
-        if (nvalid > 0) {
-          float e[RT][4];
-#pragma unroll
-          for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) e[rt][q] = __builtin_amdgcn_exp2f(x0[rt][q] - m[rt][q]);
-          weights(0, e);
-        }
+        if (nvalid > 0) vexp(0, bp);
       } else if constexpr (it > 1) {
         if (it - 1 < nvalid) vexp(it - 1, bp);
       }
@@ -1156,7 +1145,7 @@ void score1_kernel(Score1Args aa) {
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) mx[rt][q] = fmaxf(mx[rt][q], acc[0][rt][q] * c);
+        for (int q = 0; q < 4; ++q) mx[rt][q] = fmaxf(mx[rt][q], acc[0][rt][q]);
     }
     share_max(mx);
     // kb[0] is the next pass's tile 0 again, from its stage
@@ -1240,14 +1229,14 @@ void score1_kernel(Score1Args aa) {
     // element j = 2q + par of lane (gq, li) holds row (rt, 4gq + q) of tile
     // 2s + par at key li.  A operand of row tile rt: lane (gq, li) -- output
     // row li -- supplies the weight of that row to the elements of tile
-    // parity li & 1 and 0 to the others, the high fp16 part for li < 8 and
-    // the low part for li >= 8.  Output rows 4gq'+i then hold, for key li',
-    // the high (gq' < 2) or low (gq' >= 2) sum of tile 2s + (i & 1).
-    // (a lane's part of a weight goes to the low or high half of its word by
-    // a shift; lanes li < 8 take the high fp16 part, the others what it
-    // leaves)
-    const uint32_t half_shift = (uint32_t)(li & 1) * 16;
-    const bool low_part = li >= 8;
+    // parity li >> 3 and 0 to the others, the high fp16 part for even li and
+    // the low part for odd li.  Output rows 4gq'+i then hold, for key li',
+    // the high (i even) or low (i odd) sum of tile 2s + (gq' >> 1), so a lane
+    // adds its own first two results.  (A lane's part of a weight goes to
+    // the low or high half of its word by a shift; even lanes take the high
+    // fp16 part, odd lanes what it leaves.)
+    const uint32_t half_shift = (uint32_t)(li >> 3) * 16;
+    const bool low_part = (li & 1) != 0;
     const bool last_block = (blk + 1) * ROWS > R;
     auto weights_of = [&](int rt, uint32_t (&wa)[4]) __attribute__((always_inline)) {
 #pragma unroll
@@ -1267,10 +1256,10 @@ void score1_kernel(Score1Args aa) {
     };
     auto add_pair = [&](auto s_c, const floatx4& cs) __attribute__((always_inline)) {
       constexpr int sp = decltype(s_c)::value;
-      // lanes 0-31: tile 2sp, high + low; lanes 32-63: tile 2sp+1
-      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(cs[0]), __float_as_uint(cs[1]), false, false);
-      const float v = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
-      if ((gq & 1) == (sp & 1)) colacc[sp >> 1] += v;
+      // lane (gq, li): tile 2sp + (gq >> 1), high + low (added by value
+      // selection, which keeps colacc in registers)
+      const float v = cs[0] + cs[1];
+      colacc[sp >> 1] += (gq & 1) == (sp & 1) ? v : 0.f;
     };
     if constexpr (FULL) {
       // row tile by row tile: its weights, then its MFMA for every pair (one
