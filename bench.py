@@ -190,8 +190,8 @@ def summarize_pmc(fetch_csv, write_csv, workload, calib_gib):
         blob[stage] = {"kernels": kernels, "hbm_bytes_per_launch": total / passes if passes else None,
                        "sources_sha256": sources_sha256(TRAFFIC_SOURCES[stage])}
     lines += ["", "The table gives the average per dispatch.  Per pass of a stage (one scoring launch; one "
-              "selection-and-compaction pass, where the bench's staged pass runs selection as two launches and "
-              "the fused step as one):", "", "```json", json.dumps(blob, indent=1), "```"]
+              "selection-and-compaction pass, selection being one launch in the staged pass and in the fused step "
+              "alike):", "", "```json", json.dumps(blob, indent=1), "```"]
     return "\n".join(lines)
 
 
@@ -866,8 +866,8 @@ def main():
         kara.score_window(sv["params"], sv["trig"], q_v, kp, sv["bt"], sv["seq_lens"], sv["win_start"], scores,
                           sv["status"], ws, stream=stream)
         e[1].record(stream)
-        kara.select(params, scores, disc, stream=stream)
-        kara.token2chunk(params, scores, disc, kept, stream=stream)
+        # selection as the fused step runs it: discrete set and Token2Chunk in one launch
+        kara.select_kept(params, scores, disc, kept, stream=stream)
         e[2].record(stream)
         if nw == 1:
             kara.compact_pages(params, meta["trig"], kept, kp, vp, meta["bt"], meta["seq_lens"], meta["win_start"],

@@ -218,6 +218,15 @@ kara_status_t kara_token2chunk(const kara_params_t* p, int64_t n_units, const fl
                                const int32_t* discrete, int32_t* kept, void* stream);
 
 /*
+ * Eq. (5)-(8) and the fill rule of App. C.3 in one launch, as
+ * kara_compress_window runs them: writes both the discrete set (as
+ * kara_select) and the kept positions (as kara_token2chunk), bit for bit
+ * the two calls' results, with one pass over each unit's scores.
+ */
+kara_status_t kara_select_kept(const kara_params_t* p, int64_t n_units, const float* scores,
+                               int32_t* discrete, int32_t* kept, void* stream);
+
+/*
  * Window gather, Eq. (9), in place in the paged pools of n_layers layers:
  * window-relative row j receives row kept[j] for j < budget, then the buffer
  * rows, then the tail rows (each K and V head independently).  Writes status

@@ -306,6 +306,18 @@ kara_status_t kara_token2chunk(const kara_params_t* p, int64_t n_units, const fl
                                   (hipStream_t)stream));
 }
 
+kara_status_t kara_select_kept(const kara_params_t* p, int64_t n_units, const float* scores,
+                               int32_t* discrete, int32_t* kept, void* stream) {
+  Geom g;
+  kara_status_t st = make_geom(p, 0, &g);
+  if (st != KARA_OK) return st;
+  if (n_units < 0 || n_units > INT32_MAX) return KARA_ERR_INVALID_ARG;
+  if (n_units == 0) return KARA_OK;
+  if (!scores || !discrete || !kept) return KARA_ERR_INVALID_ARG;
+  return hip_status(launch_select(g, n_units, kSelectDiscrete | kSelectKept, scores, nullptr, discrete, kept,
+                                  (hipStream_t)stream));
+}
+
 kara_status_t kara_compact_pages(const kara_params_t* p, int32_t n_trig, const int32_t* trig,
                                  int32_t n_layers, const int32_t* kept, void* const* k_pools,
                                  void* const* v_pools, const int32_t* block_table,

@@ -122,6 +122,7 @@ _SIGS = {
                                  ctypes.c_size_t, _VP]),
     "kara_select": (_I32, [_PAR, ctypes.c_int64, _VP, _VP, _VP]),
     "kara_token2chunk": (_I32, [_PAR, ctypes.c_int64, _VP, _VP, _VP, _VP]),
+    "kara_select_kept": (_I32, [_PAR, ctypes.c_int64, _VP, _VP, _VP, _VP]),
     "kara_compact_pages": (_I32, [_PAR, _I32, _VP, _I32, _VP, _PP, _PP, _VP, _VP, _VP, _VP, _VP]),
     "kara_commit_tables": (_I32, [_PAR, _I32, _VP, _VP, _VP, _VP, _VP, _VP, _VP, _VP]),
     "kara_compress_window": (_I32, [_PAR, _I32, _VP, _I32, _VP, _PP, _PP, _VP, _VP, _VP, _I32, _VP, _VP,
@@ -317,6 +318,13 @@ def token2chunk(p, scores, discrete, kept, stream=None):
     n_units = scores.numel() // (p.window - p.buffer)
     _step_outputs(p, n_units, scores, discrete, kept)
     _check("kara_token2chunk", load().kara_token2chunk(ctypes.byref(p), n_units, _ptr(scores), _ptr(discrete),
+                                                       _ptr(kept), _stream(stream)))
+
+
+def select_kept(p, scores, discrete, kept, stream=None):
+    n_units = scores.numel() // (p.window - p.buffer)
+    _step_outputs(p, n_units, scores, discrete, kept)
+    _check("kara_select_kept", load().kara_select_kept(ctypes.byref(p), n_units, _ptr(scores), _ptr(discrete),
                                                        _ptr(kept), _stream(stream)))
 
 

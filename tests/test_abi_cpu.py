@@ -29,8 +29,8 @@ def good_params(**kw):
 
 def test_exports_every_declared_function(lib):
     names = kara.header_functions()
-    # 14 in kara.h, 3 in kara_harness.h, 9 in kara_sched.h, 3 in kara_recompute.h
-    assert len(names) == 29, names
+    # 15 in kara.h, 3 in kara_harness.h, 9 in kara_sched.h, 3 in kara_recompute.h
+    assert len(names) == 30, names
     for n in names:
         assert hasattr(lib, n), n
 
@@ -96,6 +96,7 @@ def test_null_pointers_rejected_before_launch(lib):
     assert lib.kara_validate(r, 4, None, None, None, None, None, None) == kara.ERR_INVALID_ARG
     assert lib.kara_select(r, 4, None, None, None) == kara.ERR_INVALID_ARG
     assert lib.kara_token2chunk(r, 4, None, None, None, None) == kara.ERR_INVALID_ARG
+    assert lib.kara_select_kept(r, 4, None, None, None, None) == kara.ERR_INVALID_ARG
     assert lib.kara_commit_tables(r, 4, None, None, None, None, None, None, None, None) == kara.ERR_INVALID_ARG
     assert lib.kara_compact_pages(r, 4, None, 1, None, None, None, None, None, None, None, None) == kara.ERR_INVALID_ARG
     assert lib.kara_score_window(r, 4, None, 1, None, None, None, None, None, None, None, None, 0, None) == kara.ERR_INVALID_ARG
@@ -105,6 +106,7 @@ def test_null_pointers_rejected_before_launch(lib):
     assert lib.kara_select(r, 0, None, None, None) == kara.OK
     assert lib.kara_validate(r, 0, None, None, None, None, None, None) == kara.OK
     assert lib.kara_token2chunk(r, 0, None, None, None, None) == kara.OK
+    assert lib.kara_select_kept(r, 0, None, None, None, None) == kara.OK
     assert lib.kara_commit_tables(r, 0, None, None, None, None, None, None, None, None) == kara.OK
     assert lib.kara_compact_pages(r, 0, None, 1, None, None, None, None, None, None, None, None) == kara.OK
     assert lib.kara_score_window(r, 0, None, 1, None, None, None, None, None, None, None, None, 0, None) == kara.OK

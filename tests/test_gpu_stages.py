@@ -1,6 +1,6 @@
 """GPU parity of each C-ABI entry point on its own, fed the oracle's output
 of the previous stage: kara_score_window (tolerance), kara_select and
-kara_token2chunk (bit-exact on given scores, including ties, negative
+kara_token2chunk and kara_select_kept (bit-exact on given scores, including ties, negative
 values and -0), kara_compact_pages and kara_commit_tables (bit-exact), plus
 the library's handling of malformed caller input."""
 import numpy as np
@@ -80,12 +80,18 @@ def test_select_and_token2chunk_bit_exact(name, scores):
         kept = torch.full((scores.shape[0], budget), -9, dtype=torch.int32, device="cuda")
         kara.select(par, sc, disc)
         kara.token2chunk(par, sc, disc, kept)
+        # the one-launch form the fused step runs
+        disc1, kept1 = torch.full_like(disc, -9), torch.full_like(kept, -9)
+        kara.select_kept(par, sc, disc1, kept1)
         torch.cuda.synchronize()
         d, k = disc.cpu().numpy(), kept.cpu().numpy()
+        d1, k1 = disc1.cpu().numpy(), kept1.cpu().numpy()
         for u in range(scores.shape[0]):
             wd, wk = oracle.kept_set(scores[u], budget, alpha, gamma)
             assert np.array_equal(d[u], wd), (name, budget, alpha, gamma, u)
             assert np.array_equal(k[u], wk), (name, budget, alpha, gamma, u)
+            assert np.array_equal(d1[u], wd), ("one launch", name, budget, alpha, gamma, u)
+            assert np.array_equal(k1[u], wk), ("one launch", name, budget, alpha, gamma, u)
 
 
 def test_token2chunk_rejects_bad_discrete():
