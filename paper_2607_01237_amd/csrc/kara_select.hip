@@ -22,7 +22,7 @@ constexpr uint32_t kArgmaxMax = 8;   // selections of at most this many items us
 struct SelFixed {
   uint32_t hist[kSelWaves][256];     // one radix histogram per wave (less atomic contention)
   uint32_t wsum[kSelWaves];
-  uint32_t bc[2];
+  uint32_t bc[3];   // radix select: the K-th key's bin, items still needed from it, items in it
   uint64_t best_key[2][kSelWaves];   // argmax rounds: per-wave best, double-buffered
   int32_t best_pos[2][kSelWaves];
 };
@@ -127,7 +127,9 @@ __device__ uint32_t block_excl_scan(uint32_t v, SelFixed& f, uint32_t* total) {
 // Marks in sel[] the K best eligible items -- larger key first, lower
 // position first among equal keys -- where thread i owns positions
 // [i*ept, i*ept+ept).  MSB-first radix select over 8-bit digits finds the
-// K-th key; items equal to it are then taken in position order.
+// K-th key; items equal to it are then taken in position order.  When the
+// K-th key's bin holds exactly the items still needed, every item of the
+// bin is selected and the lower digits need no pass.
 template <int EPT, typename KeyT>
 __device__ void radix_top(const KeyT (&key)[EPT], const bool (&elig)[EPT], bool (&sel)[EPT],
                           uint32_t K, SelFixed& f) {
@@ -136,6 +138,7 @@ __device__ void radix_top(const KeyT (&key)[EPT], const bool (&elig)[EPT], bool 
   const int wave = tid >> 6;
   KeyT prefix = 0;
   uint32_t remaining = K;
+  int whole_bin = -1;   // the digit shift of a bin taken whole, if any
   for (int shift = kBits - 8; shift >= 0; shift -= 8) {
 #pragma unroll
     for (int w = 0; w < kSelWaves; ++w) f.hist[w][tid] = 0;
@@ -168,11 +171,23 @@ __device__ void radix_top(const KeyT (&key)[EPT], const bool (&elig)[EPT], bool 
     if (above < remaining && above + h >= remaining) {
       f.bc[0] = b;
       f.bc[1] = remaining - above;
+      f.bc[2] = h;
     }
     __syncthreads();
     prefix |= (KeyT)f.bc[0] << shift;
     remaining = f.bc[1];
+    const bool whole = f.bc[2] == remaining;   // the same in every thread
     __syncthreads();
+    if (whole) {
+      whole_bin = shift;
+      break;
+    }
+  }
+  if (whole_bin >= 0) {
+    // the items above the bin and the whole bin: top digits >= the prefix's
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) sel[e] = elig[e] && (key[e] >> whole_bin) >= (prefix >> whole_bin);
+    return;
   }
   uint32_t eq = 0;
 #pragma unroll
