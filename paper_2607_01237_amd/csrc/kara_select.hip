@@ -18,11 +18,14 @@ constexpr int kSelEptMax = KARA_MAX_COMPRESSIBLE / kSelThreads;  // positions pe
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr uint32_t kArgmaxMax = 8;   // selections of at most this many items use argmax rounds
 
-// Fixed part of the LDS; the unit's arrays follow it, sized by N.
+// Fixed part of the LDS; the unit's arrays follow it, sized by N and by the
+// discrete set's size.
 struct SelFixed {
-  uint32_t hist[kSelWaves][256];     // one radix histogram per wave (less atomic contention)
+  // radix histograms, one per wave (less atomic contention), in three
+  // buffers: pass p counts into buffer p % 3 while the buffer of pass p + 2
+  // is cleared, so a pass needs one barrier
+  uint32_t hist[3][kSelWaves][256];
   uint32_t wsum[kSelWaves];
-  uint32_t bc[3];   // radix select: the K-th key's bin, items still needed from it, items in it
   uint64_t best_key[2][kSelWaves];   // argmax rounds: per-wave best, double-buffered
   int32_t best_pos[2][kSelWaves];
 };
@@ -30,13 +33,13 @@ struct SelFixed {
 struct SelSmem {
   SelFixed* f;
   float* a;          // [N] scores
-  int32_t* disc;     // [N] discrete positions, ascending
+  int32_t* disc;     // [k] discrete positions, ascending
   uint8_t* mark;     // [N] bit0 discrete, bit1 chunk interior, bit2 fill
 };
 
 __host__ __device__ constexpr size_t align16(size_t x) { return (x + 15) & ~(size_t)15; }
-__host__ __device__ inline size_t sel_lds_bytes(int N) {
-  return align16(sizeof(SelFixed)) + align16((size_t)N * 4) * 2 + align16((size_t)N);
+__host__ __device__ inline size_t sel_lds_bytes(int N, int k) {
+  return align16(sizeof(SelFixed)) + align16((size_t)N * 4) + align16((size_t)k * 4) + align16((size_t)N);
 }
 
 // Order-preserving maps to unsigned keys (larger value -> larger key); -0
@@ -135,14 +138,17 @@ __device__ void radix_top(const KeyT (&key)[EPT], const bool (&elig)[EPT], bool 
                           uint32_t K, SelFixed& f) {
   constexpr int kBits = sizeof(KeyT) * 8;
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = tid >> 6, lane = tid & 63;
+  // the first two passes' histograms start cleared
+  *(uint4*)&f.hist[0][tid >> 6][(tid & 63) * 4] = uint4{0u, 0u, 0u, 0u};
+  *(uint4*)&f.hist[1][tid >> 6][(tid & 63) * 4] = uint4{0u, 0u, 0u, 0u};
+  __syncthreads();
   KeyT prefix = 0;
   uint32_t remaining = K;
   int whole_bin = -1;   // the digit shift of a bin taken whole, if any
-  for (int shift = kBits - 8; shift >= 0; shift -= 8) {
-#pragma unroll
-    for (int w = 0; w < kSelWaves; ++w) f.hist[w][tid] = 0;
-    __syncthreads();
+  int pass = 0;
+  for (int shift = kBits - 8; shift >= 0; shift -= 8, ++pass) {
+    uint32_t(&hist)[kSelWaves][256] = f.hist[pass % 3];
     // a thread's positions often share a digit (the top digits of nearby
     // scores): add runs of equal digits with one atomic
     uint32_t run_bin = 0, run = 0;
@@ -155,30 +161,53 @@ __device__ void radix_top(const KeyT (&key)[EPT], const bool (&elig)[EPT], bool 
       if (run && b == run_bin) {
         ++run;
       } else {
-        if (run) atomicAdd(&f.hist[wave][run_bin], run);
+        if (run) atomicAdd(&hist[wave][run_bin], run);
         run_bin = b;
         run = 1;
       }
     }
-    if (run) atomicAdd(&f.hist[wave][run_bin], run);
+    if (run) atomicAdd(&hist[wave][run_bin], run);
     __syncthreads();
-    const uint32_t b = 255u - tid;   // thread i looks at bin 255-i
-    uint32_t h = 0;
+    // Every wave scans all 256 bins, largest first (lane l holds bins
+    // 255 - 4l down to 252 - 4l), and finds the bin of the remaining-th
+    // item itself: the same result in every wave, with no exchange.
+    const int b0 = 252 - 4 * lane;
+    uint4 c = {0u, 0u, 0u, 0u};
 #pragma unroll
-    for (int w = 0; w < kSelWaves; ++w) h += f.hist[w][b];
-    uint32_t tot;
-    const uint32_t above = block_excl_scan(h, f, &tot);   // items in bins > b
-    if (above < remaining && above + h >= remaining) {
-      f.bc[0] = b;
-      f.bc[1] = remaining - above;
-      f.bc[2] = h;
+    for (int w = 0; w < kSelWaves; ++w) {
+      const uint4 v = *(const uint4*)&hist[w][b0];
+      c.x += v.x;
+      c.y += v.y;
+      c.z += v.z;
+      c.w += v.w;
     }
-    __syncthreads();
-    prefix |= (KeyT)f.bc[0] << shift;
-    remaining = f.bc[1];
-    const bool whole = f.bc[2] == remaining;   // the same in every thread
-    __syncthreads();
-    if (whole) {
+    // the buffer of pass + 2 was last read by pass - 1, before this pass's barrier
+    *(uint4*)&f.hist[(pass + 2) % 3][tid >> 6][(tid & 63) * 4] = uint4{0u, 0u, 0u, 0u};
+    const uint32_t tot = c.x + c.y + c.z + c.w;
+    const uint32_t incl = wave_incl_scan(tot);
+    const uint32_t above = incl - tot;   // items in the bins above this lane's
+    const bool holder = above < remaining && remaining <= incl;
+    uint32_t bin = 0, need = 0, in_bin = 0;
+    if (holder) {
+      uint32_t a = above;
+      if (remaining <= a + c.w) {
+        bin = b0 + 3, need = remaining - a, in_bin = c.w;
+      } else if (a += c.w, remaining <= a + c.z) {
+        bin = b0 + 2, need = remaining - a, in_bin = c.z;
+      } else if (a += c.z, remaining <= a + c.y) {
+        bin = b0 + 1, need = remaining - a, in_bin = c.y;
+      } else {
+        a += c.y;
+        bin = b0, need = remaining - a, in_bin = c.x;
+      }
+    }
+    const int src = (int)__builtin_ctzll(__ballot(holder));
+    bin = (uint32_t)__builtin_amdgcn_readlane((int)bin, src);
+    need = (uint32_t)__builtin_amdgcn_readlane((int)need, src);
+    in_bin = (uint32_t)__builtin_amdgcn_readlane((int)in_bin, src);
+    prefix |= (KeyT)bin << shift;
+    remaining = need;
+    if (in_bin == need) {   // (uniform)
       whole_bin = shift;
       break;
     }
@@ -290,7 +319,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   sm.f = (SelFixed*)sel_lds;
   sm.a = (float*)(sel_lds + align16(sizeof(SelFixed)));
   sm.disc = (int32_t*)((char*)sm.a + align16((size_t)N * 4));
-  sm.mark = (uint8_t*)((char*)sm.disc + align16((size_t)N * 4));
+  sm.mark = (uint8_t*)((char*)sm.disc + align16((size_t)g.k_disc * 4));
   SelFixed& f = *sm.f;
 
   const int64_t u = blockIdx.x;
@@ -426,11 +455,11 @@ hipError_t launch_select(const Geom& g, int64_t n_units, int mode, const float* 
                          hipStream_t stream) {
   if (n_units <= 0) return hipSuccess;
   if (g.N <= 8 * kSelThreads)
-    hipLaunchKernelGGL(select_kernel<8>, dim3((unsigned)n_units), dim3(kSelThreads), sel_lds_bytes(g.N), stream, g,
-                       mode, scores, discrete_in, discrete_out, kept_out);
+    hipLaunchKernelGGL(select_kernel<8>, dim3((unsigned)n_units), dim3(kSelThreads), sel_lds_bytes(g.N, g.k_disc), stream,
+                       g, mode, scores, discrete_in, discrete_out, kept_out);
   else
-    hipLaunchKernelGGL(select_kernel<kSelEptMax>, dim3((unsigned)n_units), dim3(kSelThreads), sel_lds_bytes(g.N),
-                       stream, g, mode, scores, discrete_in, discrete_out, kept_out);
+    hipLaunchKernelGGL(select_kernel<kSelEptMax>, dim3((unsigned)n_units), dim3(kSelThreads),
+                       sel_lds_bytes(g.N, g.k_disc), stream, g, mode, scores, discrete_in, discrete_out, kept_out);
   return hipGetLastError();
 }
 
