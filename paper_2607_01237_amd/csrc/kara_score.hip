@@ -704,6 +704,86 @@ __device__ __forceinline__ void dpp_reduce16xn(float (&v)[N]) {
 #undef S1_DPP_ALL
 #undef S1_DPP16
 #undef S1_DPP8
+// Reduce-scatter over the 16 lanes of a row: every lane's v[i] combined,
+// lane li ending with index li's result.  Four butterfly steps, each
+// keeping half of the values: lanes li and li ^ 8 (a rotation by 8), then
+// li and 7 - li within each half (the half mirror), then the quad swaps
+// li ^ 2 and li ^ 1.  A lane keeps the half its bit names and sends the
+// other, so each step combines only the values that stay: 45 instructions
+// against 64 for every lane's full result.
+// (each step is one asm statement that starts with the wait states a DPP
+// read needs after the VALU writes of its sources, which all precede it)
+template <bool MAX, int K, int PATTERN>
+__device__ __forceinline__ void s1_rs_step(float (&keep)[8], const float (&send)[8]) {
+  // PATTERN: 0 row_ror:8, 1 row_half_mirror, 2 quad_perm:[2,3,0,1], 3 quad_perm:[1,0,3,2]
+#define S1_OPS(OP, PAT)                                                                                     \
+  if constexpr (K == 8)                                                                                     \
+    asm volatile("s_nop 1\n\t"                                                                              \
+                 OP " %0, %8, %0 " PAT "\n\t" OP " %1, %9, %1 " PAT "\n\t" OP " %2, %10, %2 " PAT "\n\t"    \
+                 OP " %3, %11, %3 " PAT "\n\t" OP " %4, %12, %4 " PAT "\n\t" OP " %5, %13, %5 " PAT "\n\t"  \
+                 OP " %6, %14, %6 " PAT "\n\t" OP " %7, %15, %7 " PAT                                     \
+                 : "+v"(keep[0]), "+v"(keep[1]), "+v"(keep[2]), "+v"(keep[3]), "+v"(keep[4]), "+v"(keep[5]), \
+                   "+v"(keep[6]), "+v"(keep[7])                                                             \
+                 : "v"(send[0]), "v"(send[1]), "v"(send[2]), "v"(send[3]), "v"(send[4]), "v"(send[5]),     \
+                   "v"(send[6]), "v"(send[7]));                                                             \
+  else if constexpr (K == 4)                                                                                \
+    asm volatile("s_nop 1\n\t"                                                                              \
+                 OP " %0, %4, %0 " PAT "\n\t" OP " %1, %5, %1 " PAT "\n\t" OP " %2, %6, %2 " PAT "\n\t"     \
+                 OP " %3, %7, %3 " PAT                                                                      \
+                 : "+v"(keep[0]), "+v"(keep[1]), "+v"(keep[2]), "+v"(keep[3])                               \
+                 : "v"(send[0]), "v"(send[1]), "v"(send[2]), "v"(send[3]));                                 \
+  else if constexpr (K == 2)                                                                                \
+    asm volatile("s_nop 1\n\t" OP " %0, %2, %0 " PAT "\n\t" OP " %1, %3, %1 " PAT                           \
+                 : "+v"(keep[0]), "+v"(keep[1])                                                             \
+                 : "v"(send[0]), "v"(send[1]));                                                             \
+  else                                                                                                      \
+    asm volatile("s_nop 1\n\t" OP " %0, %1, %0 " PAT : "+v"(keep[0]) : "v"(send[0]))
+  if constexpr (MAX) {
+    if constexpr (PATTERN == 0) S1_OPS("v_max_f32_dpp", "row_ror:8 row_mask:0xf bank_mask:0xf");
+    else if constexpr (PATTERN == 1) S1_OPS("v_max_f32_dpp", "row_half_mirror row_mask:0xf bank_mask:0xf");
+    else if constexpr (PATTERN == 2) S1_OPS("v_max_f32_dpp", "quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf");
+    else S1_OPS("v_max_f32_dpp", "quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf");
+  } else {
+    if constexpr (PATTERN == 0) S1_OPS("v_add_f32_dpp", "row_ror:8 row_mask:0xf bank_mask:0xf");
+    else if constexpr (PATTERN == 1) S1_OPS("v_add_f32_dpp", "row_half_mirror row_mask:0xf bank_mask:0xf");
+    else if constexpr (PATTERN == 2) S1_OPS("v_add_f32_dpp", "quad_perm:[2,3,0,1] row_mask:0xf bank_mask:0xf");
+    else S1_OPS("v_add_f32_dpp", "quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf");
+  }
+#undef S1_OPS
+}
+template <bool MAX>
+__device__ __forceinline__ float reduce_scatter16(const float (&v)[16], int li) {
+  float keep[8], send[8];
+  const bool h3 = (li & 8) != 0, h2 = (li & 4) != 0, h1 = (li & 2) != 0, h0 = (li & 1) != 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    keep[k] = h3 ? v[8 + k] : v[k];
+    send[k] = h3 ? v[k] : v[8 + k];
+  }
+  s1_rs_step<MAX, 8, 0>(keep, send);
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float a = keep[k], b = keep[4 + k];
+    keep[k] = h2 ? b : a;
+    send[k] = h2 ? a : b;
+  }
+  s1_rs_step<MAX, 4, 1>(keep, send);
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const float a = keep[k], b = keep[2 + k];
+    keep[k] = h1 ? b : a;
+    send[k] = h1 ? a : b;
+  }
+  s1_rs_step<MAX, 2, 2>(keep, send);
+  {
+    const float a = keep[0], b = keep[1];
+    keep[0] = h0 ? b : a;
+    send[0] = h0 ? a : b;
+  }
+  s1_rs_step<MAX, 1, 3>(keep, send);
+  return keep[0];
+}
+
 // max of three, with no quieting of its operands
 __device__ __forceinline__ float s1_max3(float a, float b, float c) {
   float r;
@@ -1031,18 +1111,24 @@ void score1_kernel(Score1Args aa) {
   // row reference from every wave's maxima mx of the raw logits, per lane
   // (c > 0, so the maximum of x = logit * c is c times theirs)
   auto share_max = [&](float (&mx)[RT][4]) __attribute__((always_inline)) {
-    if constexpr (RT == 4 || RT == 2) {
-      dpp_reduce16xn<true, RT * 4>(reinterpret_cast<float(&)[RT * 4]>(mx));
+    if constexpr (RT == 4) {
+      // lane li holds row (li >> 2, 4gq + (li & 3))'s maximum
+      smax[kq][rbase + (li >> 2) * 16 + 4 * gq + (li & 3)] =
+          reduce_scatter16<true>(reinterpret_cast<float(&)[16]>(mx), li);
     } else {
+      if constexpr (RT == 2) {
+        dpp_reduce16xn<true, RT * 4>(reinterpret_cast<float(&)[RT * 4]>(mx));
+      } else {
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
+        for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) mx[rt][q] = dpp_max16(mx[rt][q]);
-    }
-    if (li == 0) {
+          for (int q = 0; q < 4; ++q) mx[rt][q] = dpp_max16(mx[rt][q]);
+      }
+      if (li == 0) {
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
-        *(float4*)&smax[kq][rbase + rt * 16 + 4 * gq] = float4{mx[rt][0], mx[rt][1], mx[rt][2], mx[rt][3]};
+        for (int rt = 0; rt < RT; ++rt)
+          *(float4*)&smax[kq][rbase + rt * 16 + 4 * gq] = float4{mx[rt][0], mx[rt][1], mx[rt][2], mx[rt][3]};
+      }
     }
     lds_barrier();
 #pragma unroll
@@ -1165,29 +1251,39 @@ void score1_kernel(Score1Args aa) {
     bool m_given = false;
     for (int pass = 0; pass < 2; ++pass) {
       run_block(m_given, blk);
-      // this wave's row sums, then every wave's
-      if constexpr (RT == 4 || RT == 2) {
-        dpp_reduce16xn<false, RT * 4>(reinterpret_cast<float(&)[RT * 4]>(L));
+      // this wave's row sums, then every wave's; a wave's overflow flag:
+      // any of its row sums reached fp16's largest value (rows past R repeat
+      // row 0, so they overflow only where row 0 did)
+      bool over;
+      if constexpr (RT == 4) {
+        // lane li holds row (li >> 2, 4gq + (li & 3))'s sum
+        const float r = reduce_scatter16<false>(reinterpret_cast<float(&)[16]>(L), li);
+        ssum[kq][rbase + (li >> 2) * 16 + 4 * gq + (li & 3)] = r;
+        over = !(r < kF16Max);
       } else {
+        if constexpr (RT == 2) {
+          dpp_reduce16xn<false, RT * 4>(reinterpret_cast<float(&)[RT * 4]>(L));
+        } else {
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
+          for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) L[rt][q] = dpp_sum16(L[rt][q]);
-      }
-      if (li == 0) {
+            for (int q = 0; q < 4; ++q) L[rt][q] = dpp_sum16(L[rt][q]);
+        }
+        if (li == 0) {
 #pragma unroll
-        for (int rt = 0; rt < RT; ++rt)
-          *(float4*)&ssum[kq][rbase + rt * 16 + 4 * gq] = float4{L[rt][0], L[rt][1], L[rt][2], L[rt][3]};
-      }
-      // (rows past R repeat row 0, so they overflow only where row 0 did)
-      {
+          for (int rt = 0; rt < RT; ++rt)
+            *(float4*)&ssum[kq][rbase + rt * 16 + 4 * gq] = float4{L[rt][0], L[rt][1], L[rt][2], L[rt][3]};
+        }
         float big = L[0][0];
         static_for<1, RT * 4 / 2 + 1>([&](auto i_c) __attribute__((always_inline)) {
           constexpr int i = decltype(i_c)::value;
           constexpr int j = 2 * i - 1, k = 2 * i;
           big = s1_max3(big, L[j / 4][j % 4], L[k < RT * 4 ? k / 4 : 0][k < RT * 4 ? k % 4 : 0]);
         });
-        const bool wbad = __builtin_amdgcn_ballot_w64(!(big < kF16Max)) != 0;
+        over = !(big < kF16Max);
+      }
+      {
+        const bool wbad = __builtin_amdgcn_ballot_w64(over) != 0;
         if (lane == 0) sbad[wave] = wbad;
       }
       // the next block's queries are in LDS once the copies issued after
