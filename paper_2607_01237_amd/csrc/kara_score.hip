@@ -1258,7 +1258,7 @@ void score1_kernel(Score1Args aa) {
       if constexpr (RT == 4) {
         // lane li holds row (li >> 2, 4gq + (li & 3))'s sum
         const float r = reduce_scatter16<false>(reinterpret_cast<float(&)[16]>(L), li);
-        ssum[kq][rbase + (li >> 2) * 16 + 4 * gq + (li & 3)] = r;
+        ssum[kq][rbase + (li >> 2) * 16 + 4 * gq + (li & 3)] = r * (1.f / kS1WScale);
         over = !(r < kF16Max);
       } else {
         if constexpr (RT == 2) {
@@ -1270,9 +1270,11 @@ void score1_kernel(Score1Args aa) {
             for (int q = 0; q < 4; ++q) L[rt][q] = dpp_sum16(L[rt][q]);
         }
         if (li == 0) {
+          constexpr float s = 1.f / kS1WScale;
 #pragma unroll
           for (int rt = 0; rt < RT; ++rt)
-            *(float4*)&ssum[kq][rbase + rt * 16 + 4 * gq] = float4{L[rt][0], L[rt][1], L[rt][2], L[rt][3]};
+            *(float4*)&ssum[kq][rbase + rt * 16 + 4 * gq] =
+                float4{L[rt][0] * s, L[rt][1] * s, L[rt][2] * s, L[rt][3] * s};
         }
         float big = L[0][0];
         static_for<1, RT * 4 / 2 + 1>([&](auto i_c) __attribute__((always_inline)) {
@@ -1334,11 +1336,19 @@ void score1_kernel(Score1Args aa) {
     const uint32_t half_shift = (uint32_t)(li >> 3) * 16;
     const bool low_part = (li & 1) != 0;
     const bool last_block = (blk + 1) * ROWS > R;
+    // (the exchanged sums carry 2^-21, so 1 / sum is the scaled weight)
     auto weights_of = [&](int rt, uint32_t (&wa)[4]) __attribute__((always_inline)) {
+      float wt[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) wt[q] = __builtin_amdgcn_rcpf(ltot[rt][q]);
+      if (last_block) {   // (uniform) rows past R weigh nothing
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (blk * ROWS + rbase + rt * 16 + 4 * gq + q >= R) wt[q] = 0.f;
+      }
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const bool live = !last_block || blk * ROWS + rbase + rt * 16 + 4 * gq + q < R;
-        const float w = live ? kS1WScale * __builtin_amdgcn_rcpf(ltot[rt][q]) : 0.f;
+        const float w = wt[q];
         const float hi = (float)(_Float16)w;
         const _Float16 part = (_Float16)(w - (low_part ? hi : 0.f));
         wa[q] = (uint32_t)__builtin_bit_cast(uint16_t, part) << half_shift;
