@@ -1248,6 +1248,7 @@ void score1_kernel(Score1Args aa) {
         __builtin_memcpy(&qa[rt][ks], &v, 16);
       }
     float ltot[RT][4];
+    float lrow = 0.f;   // (four row tiles) the total of this lane's row of the reduce-scatter
     bool m_given = false;
     for (int pass = 0; pass < 2; ++pass) {
       run_block(m_given, blk);
@@ -1299,6 +1300,13 @@ void score1_kernel(Score1Args aa) {
         anybad |= f.x | f.y | f.z | f.w;
       }
       if (__builtin_amdgcn_readfirstlane(anybad) == 0) {
+        if constexpr (RT == 4) {
+          const int row = rbase + (li >> 2) * 16 + 4 * gq + (li & 3);
+          lrow = ssum[0][row];
+#pragma unroll
+          for (int w = 1; w < KQ; ++w) lrow += ssum[w][row];
+          break;
+        }
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) {
           float4 v[KQ];
@@ -1336,8 +1344,39 @@ void score1_kernel(Score1Args aa) {
     const uint32_t half_shift = (uint32_t)(li >> 3) * 16;
     const bool low_part = (li & 1) != 0;
     const bool last_block = (blk + 1) * ROWS > R;
+    // Four row tiles: each lane forms the weight of its one row of the
+    // reduce-scatter as an fp16 pair (high | low << 16), and the wave
+    // shares the pairs through its own row of smax (free until the next
+    // block's exchange; LDS operations of a wave complete in order); a
+    // lane's A-operand word is then one byte permutation of a pair.
+    uint32_t wrow[RT][4];
+    if constexpr (RT == 4) {
+      const int rrow = (li >> 2) * 16 + 4 * gq + (li & 3);   // the lane's row within the wave's rows
+      float w = __builtin_amdgcn_rcpf(lrow);
+      if (last_block && blk * ROWS + rbase + rrow >= R) w = 0.f;   // rows past R weigh nothing
+      const _Float16 hi = (_Float16)w;
+      const _Float16 lo = (_Float16)(w - (float)hi);
+      uint32_t* share = (uint32_t*)&smax[kq][rbase];
+      share[rrow] = (uint32_t)__builtin_bit_cast(uint16_t, hi) | ((uint32_t)__builtin_bit_cast(uint16_t, lo) << 16);
+      // bytes of the pair into the word: the high part (even li) or the low
+      // part (odd li), at the low (li < 8) or high half
+      const uint32_t sel = (li & 1) ? ((li >> 3) ? 0x03020c0cu : 0x0c0c0302u) : ((li >> 3) ? 0x01000c0cu : 0x0c0c0100u);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const uint4 p = *(const uint4*)&share[rt * 16 + 4 * gq];
+        wrow[rt][0] = __builtin_amdgcn_perm(p.x, p.x, sel);
+        wrow[rt][1] = __builtin_amdgcn_perm(p.y, p.y, sel);
+        wrow[rt][2] = __builtin_amdgcn_perm(p.z, p.z, sel);
+        wrow[rt][3] = __builtin_amdgcn_perm(p.w, p.w, sel);
+      }
+    }
     // (the exchanged sums carry 2^-21, so 1 / sum is the scaled weight)
     auto weights_of = [&](int rt, uint32_t (&wa)[4]) __attribute__((always_inline)) {
+      if constexpr (RT == 4) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) wa[q] = wrow[rt][q];
+        return;
+      }
       float wt[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) wt[q] = __builtin_amdgcn_rcpf(ltot[rt][q]);
