@@ -1112,9 +1112,26 @@ void score1_kernel(Score1Args aa) {
   // (c > 0, so the maximum of x = logit * c is c times theirs)
   auto share_max = [&](float (&mx)[RT][4]) __attribute__((always_inline)) {
     if constexpr (RT == 4) {
-      // lane li holds row (li >> 2, 4gq + (li & 3))'s maximum
-      smax[kq][rbase + (li >> 2) * 16 + 4 * gq + (li & 3)] =
-          reduce_scatter16<true>(reinterpret_cast<float(&)[16]>(mx), li);
+      // lane li holds row (li >> 2, 4gq + (li & 3))'s maximum: it forms that
+      // row's reference from every wave's, and the wave shares the 64
+      // through its own row of ssum (no wave reads ssum between a block's
+      // sum exchange and the next one, which this barrier precedes; LDS
+      // operations of a wave complete in order)
+      const int rrow = rbase + (li >> 2) * 16 + 4 * gq + (li & 3);
+      smax[kq][rrow] = reduce_scatter16<true>(reinterpret_cast<float(&)[16]>(mx), li);
+      lds_barrier();
+      static_assert(KQ == 4, "four key quarters");
+      const float v = s1_max3(s1_max3(smax[0][rrow], smax[1][rrow], smax[2][rrow]), smax[3][rrow], smax[3][rrow]);
+      ssum[kq][rrow] = fmaf(v, c, -kS1Headroom);
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const float4 mm = *(const float4*)&ssum[kq][rbase + rt * 16 + 4 * gq];
+        m[rt][0] = mm.x;
+        m[rt][1] = mm.y;
+        m[rt][2] = mm.z;
+        m[rt][3] = mm.w;
+      }
+      return;
     } else {
       if constexpr (RT == 2) {
         dpp_reduce16xn<true, RT * 4>(reinterpret_cast<float(&)[RT * 4]>(mx));
