@@ -1038,6 +1038,10 @@ void score1_kernel(Score1Args aa) {
   // fp16 weights in pairs of the same row from tiles 2s and 2s+1:
   // es[s][rt][q] = (row (rt, 4gq+q) at key li of tile 2s, of tile 2s+1)
   uint32_t es[NT / 2][RT][4];
+  // row-sum selector: A[M][K] = 1 where K holds row M's value (lane (gq, li),
+  // word q holds K = 8gq + 2q, +1: row 4gq + q of the pair's two tiles)
+  const uint4 rsel = {li == 4 * gq + 0 ? 0x3c003c00u : 0u, li == 4 * gq + 1 ? 0x3c003c00u : 0u,
+                      li == 4 * gq + 2 ? 0x3c003c00u : 0u, li == 4 * gq + 3 ? 0x3c003c00u : 0u};
   float ep[RT][4];        // weights of the even tile of the pair in progress
   float colacc[NT / 4];
 #pragma unroll
@@ -1068,21 +1072,30 @@ void score1_kernel(Score1Args aa) {
       for (int rt = 0; rt < RT; ++rt) acc[b][rt] = floatx4{kNegInf, kNegInf, kNegInf, kNegInf};
     }
   };
-  // a finished pair: round to fp16, add both to the row sums (one packed
-  // dot product per pair) and store
+  // a finished pair: round to fp16, add both to the row sums and store.  The
+  // row sums are a matrix product too: with the selector as A, output row M
+  // of the pair's operand is the sum of row M's two values in every key
+  // column, accumulated over the block in L (the lane's rows and keys of the
+  // logits' layout), one MFMA per row tile in place of four dot products
   auto finish_pair = [&](int sp, const float (&eo)[RT][4]) __attribute__((always_inline)) {
-    const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
+    for (int rt = 0; rt < RT; ++rt) {
+      uint32_t hp[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) hp[q] = s1_pack(ep[rt][q], eo[rt][q]);
+      const uint4 bv = {hp[0], hp[1], hp[2], hp[3]};
+      const floatx4 s = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, rsel),
+                                                               __builtin_bit_cast(f16x8, bv),
+                                                               floatx4{L[rt][0], L[rt][1], L[rt][2], L[rt][3]}, 0, 0, 0);
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const uint32_t hp = s1_pack(ep[rt][q], eo[rt][q]);
-        L[rt][q] = __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, hp), ones, L[rt][q], false);
+        L[rt][q] = s[q];
         // one wave per SIMD keeps them in accumulation registers; with two
         // waves (256 registers each) everything fits the ordinary ones
-        if constexpr (CF::kAgpr) es[sp][rt][q] = s1_to_agpr(hp);
-        else es[sp][rt][q] = hp;
+        if constexpr (CF::kAgpr) es[sp][rt][q] = s1_to_agpr(hp[q]);
+        else es[sp][rt][q] = hp[q];
       }
+    }
   };
   // weights of tile `tile` from x = logit * c - m (given as e's exponent)
   auto weights = [&](int tile, const float (&e)[RT][4]) __attribute__((always_inline)) {
@@ -1274,7 +1287,9 @@ void score1_kernel(Score1Args aa) {
       // row 0, so they overflow only where row 0 did)
       bool over;
       if constexpr (RT == 4) {
-        // lane li holds row (li >> 2, 4gq + (li & 3))'s sum
+        // lane li holds row (li >> 2, 4gq + (li & 3))'s sum (NaN, never
+        // below fp16's largest value, where the selector product met an
+        // infinity)
         const float r = reduce_scatter16<false>(reinterpret_cast<float(&)[16]>(L), li);
         ssum[kq][rbase + (li >> 2) * 16 + 4 * gq + (li & 3)] = r * (1.f / kS1WScale);
         over = !(r < kF16Max);
@@ -1294,13 +1309,14 @@ void score1_kernel(Score1Args aa) {
             *(float4*)&ssum[kq][rbase + rt * 16 + 4 * gq] =
                 float4{L[rt][0] * s, L[rt][1] * s, L[rt][2] * s, L[rt][3] * s};
         }
-        float big = L[0][0];
-        static_for<1, RT * 4 / 2 + 1>([&](auto i_c) __attribute__((always_inline)) {
-          constexpr int i = decltype(i_c)::value;
-          constexpr int j = 2 * i - 1, k = 2 * i;
-          big = s1_max3(big, L[j / 4][j % 4], L[k < RT * 4 ? k / 4 : 0][k < RT * 4 ? k % 4 : 0]);
-        });
-        over = !(big < kF16Max);
+        // (each sum on its own: a row tile's sums are all NaN where two of
+        // its values overflowed, 0 times infinity in the selector product,
+        // and a maximum would pass over them)
+        over = false;
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) over |= !(L[rt][q] < kF16Max);
       }
       {
         const bool wbad = __builtin_amdgcn_ballot_w64(over) != 0;
