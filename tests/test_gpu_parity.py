@@ -178,3 +178,10 @@ def test_kvllm_serving_geometry():
     # three blocks with a 32-token buffer, 225 kept + 32 buffer = 257 retained
     _run(ki.workload("batch8", n_seqs=3, n_layers=2, block_size=256, window=768, buffer=32, budget=225,
                      prefix=(0, 600), tail=(0, 255), num_pages=40))
+
+
+def test_wide_block_table():
+    # a block-table row wider than compaction stages in LDS (8,192 words with
+    # the kept rows): the instance that reads the kept indices and the table
+    # from global memory for every tile
+    _, rep, _ = _run(ki.workload("batch8", n_seqs=2, n_layers=2, max_blocks=8400))
