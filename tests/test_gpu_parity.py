@@ -139,7 +139,7 @@ def test_outlier_keys(pos, scale):
     # Positive: its logits lie far above the maximum of the row's first keys,
     # where the scoring kernel takes its reference, and it takes nearly all
     # the probability of the rows it agrees with.  Its fp16 weights overflow
-    # in about half the rows of every row tile, so the row sums' selector
+    # in roughly a third of the rows of every row tile, so the row sums' selector
     # products meet infinities (0 * inf: whole row tiles of NaN sums) and the
     # overflow redo has to take NaN as overflow.  Negative: its probabilities
     # sit tens of binades below the row maxima.
