@@ -600,7 +600,9 @@ __global__ __launch_bounds__(256) void split_sum_kernel(const float* __restrict_
 // first tiles' logits less kS1Headroom, exchanged once per block through
 // LDS.  When the row sums are known, the weights 1/L (one per row, the same
 // for every wave since m is shared) are applied by fp16 MFMAs of the stored
-// values, 32 rows at a time, which sums each key's column.  The keys of a
+// values, 32 rows at a time, which sums each key's column; the row sums
+// themselves accumulate on the matrix cores too, each tile pair's stored
+// values times a constant 0/1 selector.  The keys of a
 // wave stream through its own LDS ring by direct global->LDS copies, the
 // same keys for every block of the unit, so the ring runs on across blocks
 // and no workgroup barrier guards it; the next block's queries are copied
@@ -613,7 +615,8 @@ __global__ __launch_bounds__(256) void split_sum_kernel(const float* __restrict_
 // is 64, so a term of fp16's subnormal range contributes at most 2^-31 to a
 // probability.  A row whose later logits rise more than about 10 log2 units
 // above its first tiles' maximum would overflow fp16: any wave's row sum
-// reaching 65504 (which every overflowing term would exceed) sends the block
+// reaching 65504 (which every overflowing term would exceed) or NaN (where
+// the selector's zeros met an infinity) sends the block
 // through once more with m = (exact row maximum) - 6, where no term exceeds
 // 64 and no wave sum 64 * 512.
 // ---------------------------------------------------------------------------
@@ -1076,7 +1079,7 @@ void score1_kernel(Score1Args aa) {
   // row sums are a matrix product too: with the selector as A, output row M
   // of the pair's operand is the sum of row M's two values in every key
   // column, accumulated over the block in L (the lane's rows and keys of the
-  // logits' layout), one MFMA per row tile in place of four dot products
+  // logits' layout): one MFMA per row tile and tile pair
   auto finish_pair = [&](int sp, const float (&eo)[RT][4]) __attribute__((always_inline)) {
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
