@@ -133,6 +133,17 @@ def test_maximum_compressible_window(window, buffer):
     _run(cfg)
 
 
+
+@pytest.mark.parametrize("window", [600, 1000, 1300, 1536, 2048])
+def test_single_sweep_instances(window):
+    # bf16, d = 128: every instance of the single-sweep scoring kernel, by
+    # key tiles per wave (16, 24, 32) and whole or ragged tiles: N = 600 and
+    # 1000 (16, ragged), 1300 (24, ragged), 1536 (24, whole), 2048 (32, whole)
+    cfg = ki.workload("batch8", n_seqs=2, n_layers=1, n_q_heads=4, n_kv_heads=1, window=window,
+                      budget=window // 5, prefix=(0, 100), tail=(0, 9), num_pages=600, key_mode="normal")
+    _run(cfg)
+
+
 @pytest.mark.parametrize("pos,scale", [(700, 16.0), (300, 16.0), (40, 16.0), (700, -16.0)])
 def test_outlier_keys(pos, scale):
     # One window key per (sequence, head) scaled by 16 (exact in bf16).
